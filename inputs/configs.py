@@ -1,0 +1,113 @@
+"""The five synthetic workloads (grammar, vocabulary, prefixes, logits).
+
+Each prefix is drawn independently per (step, b) from a seeded random
+document of the workload's language, truncated at a uniform byte position
+(0..len inclusive), so prefixes end mid-lexeme as often as the documents'
+lexeme lengths dictate.  Everything is a pure function of the seeds.
+"""
+from __future__ import annotations
+
+import functools
+from dataclasses import dataclass
+from typing import Callable
+
+import numpy as np
+
+from . import documents, grammars, vocab
+from .grammar import GrammarTables
+from .native import HostParser
+from .seeds import rng_for
+
+
+@dataclass
+class Workload:
+    index: int                   # 0..4
+    name: str
+    B: int
+    steps: int
+    logits_dtype: str            # "f32" | "bf16"
+    logits_std: float
+    make_grammar: Callable[[], GrammarTables]
+    make_vocab: Callable[[GrammarTables], vocab.Vocab]
+    make_document: Callable[[np.random.Generator, "Workload"], bytes]
+    description: str = ""
+
+    # ---- cached pieces ----
+    @functools.cached_property
+    def grammar(self) -> GrammarTables:
+        return self.make_grammar()
+
+    @functools.cached_property
+    def vocab(self) -> vocab.Vocab:
+        return self.make_vocab(self.grammar)
+
+    @functools.cached_property
+    def host(self) -> HostParser:
+        return HostParser(self.grammar)
+
+    @property
+    def V(self) -> int:
+        return self.vocab.size
+
+    def prefix(self, step: int, b: int) -> bytes:
+        rng = rng_for(self.index, step, b)
+        doc = self.make_document(rng, self)
+        cut = int(rng.integers(0, len(doc) + 1))
+        return doc[:cut]
+
+    def states(self, step: int, B: int | None = None) -> list[tuple[int, np.ndarray]]:
+        """(q, stack) for every sequence of one decoding step."""
+        B = self.B if B is None else B
+        return [self.host.state(self.prefix(step, b)) for b in range(B)]
+
+    def logits(self, step: int, B: int | None = None):
+        """Seeded logits as a CPU torch tensor [B, V]."""
+        import torch
+        B = self.B if B is None else B
+        gen = torch.Generator().manual_seed(0x50534300 + self.index * 1_000_003 + step)
+        x = torch.randn(B, self.V, generator=gen, dtype=torch.float32) * self.logits_std
+        return x.to(torch.bfloat16) if self.logits_dtype == "bf16" else x
+
+
+def _arith_doc(rng, wl):
+    return documents.arithmetic_document(rng, max_depth=12)
+
+
+@functools.lru_cache(maxsize=None)
+def _json_words():
+    return vocab.synthetic_words(rng_for(1, salt=0xD0C), 400)
+
+
+def _json_doc(rng, wl):
+    return documents.json_document(rng, _json_words(), max_depth=20)
+
+
+def _c1_vocab(g):
+    return vocab.arithmetic_vocab(rng_for(0, salt=0x70C), 513)
+
+
+def _c2_vocab(g):
+    return vocab.json_vocab(rng_for(1, salt=0x70C), 32000)
+
+
+WORKLOADS: dict[str, Workload] = {}
+
+
+def _register(w: Workload):
+    WORKLOADS[w.name] = w
+    return w
+
+
+ARITHMETIC = _register(Workload(
+    0, "arithmetic", B=1, steps=200, logits_dtype="f32", logits_std=1.0,
+    make_grammar=grammars.arithmetic, make_vocab=_c1_vocab, make_document=_arith_doc,
+    description="E->E+T|T, T->T*F|F, F->(E)|NUM, spaces; V=513; B=1; fp32 N(0,1)"))
+
+JSON = _register(Workload(
+    1, "json", B=16, steps=500, logits_dtype="f32", logits_std=1.0,
+    make_grammar=grammars.json_grammar, make_vocab=_c2_vocab, make_document=_json_doc,
+    description="JSON; byte-level V=32,000; B=16; fp32 N(0,1)"))
+
+
+def get(name: str) -> Workload:
+    return WORKLOADS[name]
