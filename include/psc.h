@@ -1,0 +1,197 @@
+/*
+ * psc.h -- C ABI of the parser-stack-classification mask library (gfx950).
+ *
+ * Grammar-constrained decoding asks, at every decoding step and for every
+ * sequence, which vocabulary tokens may follow the current prefix (the
+ * constraint c(x), Sec. 2.1, eq. cons).  Parser stack classification
+ * (Sec. 3) precomputes, once per (grammar, vocabulary) pair, one
+ * deterministic automaton that reads the lexer state q and the parser stack
+ * alpha top-first and lands in a state whose accepted vocabulary set is
+ * precomputed (Sec. 3.5, eq. final_c and the sets A_s; Algorithm 1).  At
+ * run time the automaton is walked once per sequence and the class's mask
+ * is copied out (Algorithm 2, classification and mask steps); the mask is
+ * then applied to the logits (Sec. 1, Fig. 1a).
+ *
+ * Conventions used by every call:
+ *  - All sizes are element counts unless named *_bytes.
+ *  - Masks are uint32 words, LSB-first: bit (v & 31) of word (v >> 5) is 1
+ *    iff token v is allowed.  W = ceil(V / 32) words per row; bits >= V are 0.
+ *  - Device pointers are HBM pointers owned by the caller; the library never
+ *    frees them.  `stream` is a hipStream_t passed as void* (NULL = default
+ *    stream).  Device calls only enqueue work; they never synchronise.
+ *  - Every call returns psc_status; psc_last_error() gives a thread-local
+ *    message for the last non-OK status.
+ */
+#ifndef PSC_H
+#define PSC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PSC_OK = 0,
+    PSC_E_INVALID_ARG = -1, /* null pointer, negative size, inconsistent shape */
+    PSC_E_GRAMMAR = -2,     /* malformed tables (ids out of range, empty spelling, ...) */
+    PSC_E_OOM = -4,         /* host allocation failed                                 */
+    PSC_E_DEVICE = -5,      /* a HIP call or kernel launch failed                     */
+    PSC_E_NOT_BOUND = -6,   /* device tables not bound (psc_bind_device)              */
+    PSC_E_LIMIT = -7        /* the construction exceeded a size limit                 */
+} psc_status;
+
+typedef enum { PSC_F32 = 0, PSC_BF16 = 1 } psc_dtype;
+
+/*
+ * The problem instance: the lexer T and the parser P that Algorithm 1 takes
+ * as arguments (Sec. 2.2 FST, Sec. 2.4 PDA realised as LR tables, Sec. 4.1).
+ * All arrays are host memory, row-major, read during psc_build only.
+ *
+ *  lex_next   [n_lex_states][256]  next lexer state on a byte, -1 = none.
+ *                                  State 0 is q0 ("nothing pending").
+ *  lex_accept [n_lex_states]       terminal the pending lexeme would be
+ *                                  emitted as, -1 if not accepting.  Lexing is
+ *                                  longest match with one byte of lookahead.
+ *  terminal_ignored [n_terminals]  1 = consumed by the lexer, never parsed.
+ *  end_terminal                    id of the end-of-input terminal $end.
+ *  action [n_lr_states][n_terminals] (a & 3): 0 error, 1 shift to a >> 2,
+ *                                  2 reduce by production a >> 2, 3 accept.
+ *  goto_table [n_lr_states][n_nonterminals]  -1 = none.
+ *  prod_lhs, prod_len [n_productions]        production 0 is the augmented
+ *                                  start production.
+ * Parser stacks are sequences of LR state ids (the stack alphabet Pi).
+ */
+typedef struct {
+    int32_t n_lex_states;
+    const int32_t *lex_next;
+    const int32_t *lex_accept;
+    int32_t n_terminals;
+    const uint8_t *terminal_ignored;
+    int32_t end_terminal;
+    int32_t n_lr_states;
+    int32_t n_nonterminals;
+    const int32_t *action;
+    const int32_t *goto_table;
+    int32_t n_productions;
+    const int32_t *prod_lhs;
+    const int32_t *prod_len;
+} psc_grammar;
+
+/* The vocabulary V (Sec. 2.1): token v is bytes[offsets[v] .. offsets[v+1]).
+ * Every spelling is non-empty except the EOS token's (eos_id, or -1 for
+ * none).  Host memory, read during psc_build only. */
+typedef struct {
+    int32_t n_tokens;
+    const uint8_t *bytes;
+    const int64_t *offsets; /* [n_tokens + 1] */
+    int32_t eos_id;
+} psc_vocab;
+
+typedef struct psc_handle psc_handle; /* opaque; owned by the library until psc_free */
+
+typedef struct {
+    int32_t vocab_size;        /* V                                           */
+    int32_t mask_words;        /* W = ceil(V/32)                              */
+    int32_t mask_stride_words; /* row stride of the device mask table (>= W)  */
+    int32_t n_lex_states;      /* |Q|                                         */
+    int32_t n_lr_states;       /* |Pi|                                        */
+    int32_t n_classes;         /* distinct precomputed masks (rows)           */
+    int64_t dfa_states_built;  /* automaton states before minimisation        */
+    int32_t dfa_states;        /* after minimisation                          */
+    int32_t dfa_rows;          /* states that need a row (not determined)     */
+    int32_t dense_rows;        /* rows stored densely over Pi                 */
+    int32_t max_sparse_edges;  /* largest sparse row                          */
+    int64_t table_bytes;       /* classifier table bytes on the device        */
+    int64_t mask_table_bytes;  /* mask table bytes on the device              */
+    int64_t device_bytes;      /* total device buffer needed (psc_device_bytes) */
+    double build_seconds;      /* wall time of psc_build                      */
+} psc_info_t;
+
+/*
+ * Offline construction (Algorithm 1; Sec. 3.1-3.5), CPU only.  Lexes every
+ * token from every lexer state (R_q(v), Sec. 3.1), simulates the parser on
+ * every realizable terminal sequence against a stack read lazily top-first
+ * (the transducers P_eps, P~_a and P_w of Sec. 3.3-3.4, run in lock step),
+ * determinises the union over (q, v) into one automaton (eq. final_c),
+ * minimises it, deduplicates the per-state accepted sets A_s into classes,
+ * and flattens everything into device-ready arrays.
+ * On success *out receives a new handle.  Errors: PSC_E_INVALID_ARG (null
+ * pointers, sizes <= 0), PSC_E_GRAMMAR (ids out of range, a non-EOS token with
+ * an empty spelling), PSC_E_OOM, PSC_E_LIMIT.
+ */
+psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out);
+
+/* Sizes and statistics of a built handle. */
+psc_status psc_info(const psc_handle *h, psc_info_t *out);
+
+/* Device bytes psc_bind_device needs (256-byte aligned buffer). */
+size_t psc_device_bytes(const psc_handle *h);
+
+/*
+ * Copy the classifier and mask tables into caller-allocated device memory
+ * (dev_buf, nbytes >= psc_device_bytes, 256-byte aligned) on `stream`, and
+ * zero the device error counter.  The buffer must stay alive and unmodified
+ * while the handle is used; the handle keeps only the pointer.  Rebinding
+ * replaces the previous binding.  Errors: PSC_E_INVALID_ARG, PSC_E_DEVICE.
+ */
+psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream);
+
+/*
+ * Per-step mask computation (Algorithm 2, classification and mask steps).
+ * For every sequence b < B: start from the automaton state for
+ * lexer_states[b], read its stack top-first, stop early once the class is
+ * determined, and copy that class's precomputed mask into
+ * out_bitmask[b][0..W).
+ *  stacks       device int32, the B stacks concatenated in batch order, each
+ *               stored bottom -> top (LR start state first, top last).
+ *  stack_lens   device int32 [B], each >= 1.
+ *  lexer_states device int32 [B].
+ *  out_bitmask  device uint32 [B][W], W = ceil(V/32), fully written.
+ * A sequence with an out-of-range lexer state or stack symbol, or a length
+ * <= 0, gets an all-zero row and increments the device error counter; a
+ * well-formed stack that no prefix can produce gives an unspecified row.
+ * B == 0 is a no-op.  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND, PSC_E_DEVICE.
+ */
+psc_status psc_compute_masks(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                             const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
+                             void *stream);
+
+/*
+ * Mask application (Sec. 1, Fig. 1a: logits are masked before sampling), in
+ * place on a contiguous device tensor logits[B][V] of `dtype`:
+ *   logits[b][v] = -inf   wherever bit v of bitmask[b] (uint32 [B][ceil(V/32)]) is 0;
+ * allowed entries are left untouched (their bits, NaN payloads included, do
+ * not change).  B == 0 or V == 0 is a no-op.  Errors: PSC_E_INVALID_ARG,
+ * PSC_E_DEVICE.
+ */
+psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask, int32_t B,
+                          int32_t V, void *stream);
+
+/* Read (synchronously, on `stream`) and optionally reset the device counter
+ * of sequences that psc_compute_masks rejected as out of range. */
+psc_status psc_device_error_count(const psc_handle *h, uint32_t *out, int32_t reset, void *stream);
+
+/*
+ * Host walk of the same automaton, for triage and for timing the method on
+ * one CPU thread as the paper does: classes for B host-resident prefix
+ * states (same stack layout as psc_compute_masks, host pointers).  It is not
+ * used by any device call.  out_classes[b] = -1 for an out-of-range input.
+ */
+psc_status psc_classify_host(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                             const int32_t *lexer_states, int32_t B, int32_t *out_classes);
+
+/* Copy class c's mask row (W words) to host memory. */
+psc_status psc_class_mask_host(const psc_handle *h, int32_t cls, uint32_t *out_row);
+
+/* Release the handle and its host tables (never the caller's device buffer). */
+void psc_free(psc_handle *h);
+
+/* Thread-local message for the last non-OK status of this thread. */
+const char *psc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PSC_H */

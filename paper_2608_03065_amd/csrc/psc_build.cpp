@@ -1,0 +1,929 @@
+// Offline construction of the parser-stack classifier (Algorithm 1).
+//
+// Input: the lexer T (byte DFA), the LR(1) tables realising the parser P,
+// and the vocabulary V.  Output: one deterministic automaton over the stack
+// alphabet (LR states) whose states carry precomputed token masks, flattened
+// into int32 rows, plus a deduplicated table of mask rows.
+//
+// Route.  The paper builds, for every realizable terminal sequence w, the
+// transducer P_w = P_eps o P~_w1 o P_eps o ... o P~_wn o P_eps (Sec. 3.3-3.4,
+// eq. compose), drops its outputs (A_w), unions I_q A_w I_v over all q, v and
+// w in R_q(v), then determinises and minimises (Sec. 3.5, eq. final_c).  We
+// build the same language directly in determinised form: for one lexer
+// state q at a time, a subset construction whose subset elements are the
+// "threads" of those transducers, all run in lock step while the stack is
+// read top-first:
+//   * a thread stands for one terminal-sequence prefix (a node of the trie
+//     of all sequences in R_q(V)) whose parser simulation has used up every
+//     stack symbol it knows and is waiting for the next one;
+//   * it waits either to skip k more symbols (a reduction popped below what
+//     is known, P~/P_eps "readup") and then take the goto on nonterminal A
+//     from the symbol after them, or -- the start thread -- for the top;
+//   * reading a symbol resumes every thread: reductions run while the stack
+//     they need is known (P_eps "execute"), a shift advances to the trie
+//     child (P~_a), reaching a node that ends a sequence accepts that
+//     sequence's tokens (the stack is stable right after a shift), and an
+//     error drops the thread;
+//   * a subset state is (set of waiting threads, mask of tokens accepted so
+//     far); when the stack ends, waiting threads die and the state's mask is
+//     its accepted set A_s (Sec. 3.5).
+// Realizable sequences R_q(v) = x T_p (Sec. 3.1) come from lexing each token
+// from q (longest match, one byte of lookahead), T_p being the terminals the
+// pending lexeme can still become.  The automaton is then minimised (Moore),
+// states whose class can no longer change are marked determined (walks stop
+// there), and everything is flattened for the device.
+#include <algorithm>
+#include <chrono>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <stdexcept>
+#include <unordered_map>
+
+#include "psc_internal.hpp"
+
+namespace psc {
+
+static thread_local std::string g_last_error;
+void set_error(const std::string &msg) { g_last_error = msg; }
+
+namespace {
+
+struct BuildError : std::runtime_error {
+    psc_status code;
+    BuildError(psc_status c, const std::string &m) : std::runtime_error(m), code(c) {}
+};
+
+inline uint64_t mix64(uint64_t x) {
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+
+// Interning of variable-length keys (open addressing over ids).
+template <class T>
+class Interner {
+  public:
+    int32_t find_or_add(const T *key, size_t n, bool *added) {
+        uint64_t h = hash(key, n);
+        if ((ids_.size() + 1) * 2 > slots_.size()) grow();
+        size_t mask = slots_.size() - 1;
+        size_t i = h & mask;
+        while (true) {
+            int32_t id = slots_[i];
+            if (id < 0) break;
+            if (hashes_[id] == h && len(id) == n && std::equal(key, key + n, data(id))) {
+                *added = false;
+                return id;
+            }
+            i = (i + 1) & mask;
+        }
+        int32_t id = (int32_t)ids_.size();
+        slots_[i] = id;
+        ids_.push_back(pool_.size());
+        hashes_.push_back(h);
+        pool_.insert(pool_.end(), key, key + n);
+        ends_.push_back(pool_.size());
+        *added = true;
+        return id;
+    }
+    size_t size() const { return ids_.size(); }
+    const T *data(int32_t id) const { return pool_.data() + ids_[id]; }
+    size_t len(int32_t id) const { return ends_[id] - ids_[id]; }
+    void clear() {
+        pool_.clear(); ids_.clear(); ends_.clear(); hashes_.clear();
+        slots_.assign(16, -1);
+        pool_.shrink_to_fit(); ids_.shrink_to_fit(); ends_.shrink_to_fit(); hashes_.shrink_to_fit();
+    }
+    Interner() { slots_.assign(16, -1); }
+
+  private:
+    static uint64_t hash(const T *k, size_t n) {
+        uint64_t h = 0x1234567ull + n;
+        for (size_t i = 0; i < n; i++) h = mix64(h ^ (uint64_t)k[i]);
+        return h;
+    }
+    void grow() {
+        std::vector<int32_t> ns(slots_.size() * 2, -1);
+        size_t mask = ns.size() - 1;
+        for (size_t id = 0; id < ids_.size(); id++) {
+            size_t i = hashes_[id] & mask;
+            while (ns[i] >= 0) i = (i + 1) & mask;
+            ns[i] = (int32_t)id;
+        }
+        slots_.swap(ns);
+    }
+    std::vector<T> pool_;
+    std::vector<size_t> ids_, ends_;
+    std::vector<uint64_t> hashes_;
+    std::vector<int32_t> slots_;
+};
+
+// ------------------------------------------------------------------ grammar
+
+struct Gram {
+    int32_t nQ, nT, nPi, nN, nP, endT;
+    const int32_t *lex_next, *lex_accept, *action, *go, *plhs, *plen;
+    const uint8_t *ign;
+    int32_t act(int32_t s, int32_t t) const { return action[(int64_t)s * nT + t]; }
+    int32_t gto(int32_t s, int32_t A) const { return go[(int64_t)s * nN + A]; }
+};
+
+void validate(const psc_grammar *g, const psc_vocab *v) {
+    auto bad = [](const std::string &m) { throw BuildError(PSC_E_GRAMMAR, m); };
+    if (g->n_lex_states <= 0 || g->n_terminals <= 0 || g->n_lr_states <= 0 ||
+        g->n_nonterminals <= 0 || g->n_productions <= 0)
+        throw BuildError(PSC_E_INVALID_ARG, "grammar sizes must be positive");
+    if (!g->lex_next || !g->lex_accept || !g->terminal_ignored || !g->action || !g->goto_table ||
+        !g->prod_lhs || !g->prod_len)
+        throw BuildError(PSC_E_INVALID_ARG, "null grammar array");
+    if (g->n_nonterminals >= 32767 || g->n_lr_states >= (1 << 29))
+        throw BuildError(PSC_E_LIMIT, "grammar too large for the table encoding");
+    if (g->end_terminal < 0 || g->end_terminal >= g->n_terminals) bad("end_terminal out of range");
+    if (g->lex_accept[0] != -1) bad("lexer state 0 (q0) must not be accepting");
+    for (int64_t i = 0; i < (int64_t)g->n_lex_states * 256; i++) {
+        int32_t x = g->lex_next[i];
+        if (x < -1 || x >= g->n_lex_states) bad("lexer transition out of range");
+        if (x == 0) bad("no lexer transition may lead back to q0");
+    }
+    for (int32_t i = 0; i < g->n_lex_states; i++)
+        if (g->lex_accept[i] < -1 || g->lex_accept[i] >= g->n_terminals ||
+            g->lex_accept[i] == g->end_terminal)
+            bad("lexer accept label out of range");
+    for (int32_t p = 0; p < g->n_productions; p++)
+        if (g->prod_lhs[p] < 0 || g->prod_lhs[p] >= g->n_nonterminals || g->prod_len[p] < 0)
+            bad("production out of range");
+    for (int64_t i = 0; i < (int64_t)g->n_lr_states * g->n_terminals; i++) {
+        int32_t a = g->action[i];
+        int k = a & 3;
+        if (k == 1 && ((a >> 2) < 0 || (a >> 2) >= g->n_lr_states)) bad("shift target out of range");
+        if (k == 2 && ((a >> 2) < 0 || (a >> 2) >= g->n_productions)) bad("reduce production out of range");
+        if (k == 0 && a != 0) bad("error entries must be 0");
+    }
+    for (int64_t i = 0; i < (int64_t)g->n_lr_states * g->n_nonterminals; i++)
+        if (g->goto_table[i] < -1 || g->goto_table[i] >= g->n_lr_states) bad("goto out of range");
+    if (v->n_tokens <= 0 || !v->offsets || (!v->bytes && v->offsets[v->n_tokens] > 0))
+        throw BuildError(PSC_E_INVALID_ARG, "empty or null vocabulary");
+    if (v->eos_id < -1 || v->eos_id >= v->n_tokens) throw BuildError(PSC_E_INVALID_ARG, "eos_id out of range");
+    if (v->offsets[0] != 0) bad("vocabulary offsets must start at 0");
+    for (int32_t t = 0; t < v->n_tokens; t++) {
+        int64_t n = v->offsets[t + 1] - v->offsets[t];
+        if (n < 0) bad("vocabulary offsets must be non-decreasing");
+        if (n == 0 && t != v->eos_id) bad("only the EOS token may have an empty spelling");
+        if (n > 0 && t == v->eos_id) bad("the EOS token must have an empty spelling");
+    }
+}
+
+// T_p for every lexer state p (Sec. 3.1): the terminals whose accepting
+// states are reachable from p, and whether "nothing more" is possible
+// (p == q0, or an ignored terminal is reachable).
+struct Completions {
+    std::vector<std::vector<int32_t>> terms;  // non-ignored terminals per p
+    std::vector<uint8_t> eps;
+};
+
+Completions completions(const Gram &G) {
+    int32_t words = (G.nT + 63) / 64;
+    std::vector<uint64_t> R((size_t)G.nQ * words, 0);
+    std::vector<std::vector<int32_t>> succ(G.nQ);
+    for (int32_t p = 0; p < G.nQ; p++) {
+        if (G.lex_accept[p] >= 0) R[(size_t)p * words + G.lex_accept[p] / 64] |= 1ull << (G.lex_accept[p] % 64);
+        for (int c = 0; c < 256; c++) {
+            int32_t r = G.lex_next[(int64_t)p * 256 + c];
+            if (r >= 0 && r != p) succ[p].push_back(r);
+        }
+        std::sort(succ[p].begin(), succ[p].end());
+        succ[p].erase(std::unique(succ[p].begin(), succ[p].end()), succ[p].end());
+    }
+    bool changed = true;
+    while (changed) {
+        changed = false;
+        for (int32_t p = G.nQ - 1; p >= 0; p--) {
+            uint64_t *rp = &R[(size_t)p * words];
+            for (int32_t r : succ[p]) {
+                const uint64_t *rr = &R[(size_t)r * words];
+                for (int32_t k = 0; k < words; k++) {
+                    uint64_t nv = rp[k] | rr[k];
+                    if (nv != rp[k]) { rp[k] = nv; changed = true; }
+                }
+            }
+        }
+    }
+    Completions C;
+    C.terms.resize(G.nQ);
+    C.eps.assign(G.nQ, 0);
+    for (int32_t p = 0; p < G.nQ; p++) {
+        if (p == 0) C.eps[p] = 1;
+        for (int32_t t = 0; t < G.nT; t++) {
+            if (!(R[(size_t)p * words + t / 64] >> (t % 64) & 1)) continue;
+            if (G.ign[t]) C.eps[p] = 1;
+            else C.terms[p].push_back(t);
+        }
+    }
+    return C;
+}
+
+// ------------------------------------------------------- vocabulary trie
+
+struct VocabTrie {
+    std::vector<int32_t> depth, subtree_end, tok_begin, tok_end;
+    std::vector<uint8_t> byte;
+    std::vector<int32_t> toks;   // token ids ending at nodes, grouped by node
+};
+
+VocabTrie vocab_trie(const psc_vocab *v) {
+    std::vector<int32_t> ids;
+    for (int32_t t = 0; t < v->n_tokens; t++)
+        if (t != v->eos_id) ids.push_back(t);
+    auto spell = [&](int32_t t) {
+        return std::pair<const uint8_t *, int64_t>(v->bytes + v->offsets[t], v->offsets[t + 1] - v->offsets[t]);
+    };
+    std::sort(ids.begin(), ids.end(), [&](int32_t a, int32_t b) {
+        auto [pa, na] = spell(a);
+        auto [pb, nb] = spell(b);
+        int c = std::memcmp(pa, pb, (size_t)std::min(na, nb));
+        return c != 0 ? c < 0 : (na != nb ? na < nb : a < b);
+    });
+    VocabTrie T;
+    T.depth.push_back(0);
+    T.byte.push_back(0);
+    std::vector<int32_t> node_tok_owner;  // node id per entry of toks (built in node order)
+    std::vector<std::pair<int32_t, int32_t>> ends;  // (node, token)
+    std::vector<int32_t> path{0};  // node at each depth of the previous token
+    const uint8_t *prev = nullptr;
+    int64_t prev_n = 0;
+    for (int32_t t : ids) {
+        auto [p, n] = spell(t);
+        int64_t lcp = 0;
+        if (prev) while (lcp < n && lcp < prev_n && p[lcp] == prev[lcp]) lcp++;
+        path.resize((size_t)lcp + 1);
+        for (int64_t d = lcp; d < n; d++) {
+            T.depth.push_back((int32_t)d + 1);
+            T.byte.push_back(p[d]);
+            path.push_back((int32_t)T.depth.size() - 1);
+        }
+        ends.emplace_back(path[(size_t)n], t);
+        prev = p;
+        prev_n = n;
+    }
+    int32_t N = (int32_t)T.depth.size();
+    std::sort(ends.begin(), ends.end());
+    T.tok_begin.assign(N, 0);
+    T.tok_end.assign(N, 0);
+    size_t e = 0;
+    for (int32_t i = 0; i < N; i++) {
+        T.tok_begin[i] = (int32_t)T.toks.size();
+        while (e < ends.size() && ends[e].first == i) T.toks.push_back(ends[e++].second);
+        T.tok_end[i] = (int32_t)T.toks.size();
+    }
+    T.subtree_end.assign(N, N);
+    std::vector<int32_t> open;
+    for (int32_t i = 0; i < N; i++) {
+        while (!open.empty() && T.depth[open.back()] >= T.depth[i]) {
+            T.subtree_end[open.back()] = i;
+            open.pop_back();
+        }
+        open.push_back(i);
+    }
+    return T;
+}
+
+// ----------------------------------------------------------- automaton
+
+constexpr int32_t kInitA = 0xFFFF;   // "read the top" thread marker
+
+inline uint64_t pack_thread(int32_t node, int32_t k, int32_t A) {
+    return ((uint64_t)(uint32_t)node << 32) | ((uint64_t)(uint32_t)k << 16) | (uint64_t)(uint32_t)A;
+}
+inline int32_t th_node(uint64_t t) { return (int32_t)(t >> 32); }
+inline int32_t th_k(uint64_t t) { return (int32_t)((t >> 16) & 0xFFFF); }
+inline int32_t th_A(uint64_t t) { return (int32_t)(t & 0xFFFF); }
+
+struct Builder {
+    const Gram &G;
+    const psc_vocab *vocab;
+    const Completions &C;
+    const VocabTrie &VT;
+    int32_t V, W;
+    bool verbose;
+
+    // global mask classes (class 0 = all zero)
+    Interner<uint32_t> masks;
+    // global automaton states
+    std::vector<int32_t> st_cls, st_def, st_ebeg, st_eend;
+    std::vector<int32_t> e_sym, e_tgt;
+    std::unordered_map<int32_t, int32_t> empty_state_of_cls;
+    std::vector<int32_t> start_state;   // per lexer state
+    std::vector<std::vector<int32_t>> goto_sources;  // per nonterminal
+    int64_t states_built = 0;
+
+    // per-q scratch
+    std::vector<int32_t> tn_label, tn_child_beg, tn_child_end, tn_children, tn_grp_beg, tn_grp_end, tn_grps;
+    std::vector<std::vector<int32_t>> grp_tokens;
+    Interner<uint64_t> qstates;          // key: [cls, threads...]
+    std::vector<int32_t> qstate_global;  // qstate id -> global state id
+    std::unordered_map<uint64_t, int32_t> add_memo;  // (cls, node) -> cls
+    std::vector<uint64_t> newW;
+    std::vector<int32_t> acc;
+    std::vector<uint32_t> rowbuf;
+
+    Builder(const Gram &g, const psc_vocab *v, const Completions &c, const VocabTrie &vt, bool verb)
+        : G(g), vocab(v), C(c), VT(vt), V(v->n_tokens), W((v->n_tokens + 31) / 32), verbose(verb) {
+        std::vector<uint32_t> zero(W, 0);
+        bool added;
+        masks.find_or_add(zero.data(), W, &added);
+        goto_sources.resize(G.nN);
+        for (int32_t s = 0; s < G.nPi; s++)
+            for (int32_t A = 0; A < G.nN; A++)
+                if (G.gto(s, A) >= 0) goto_sources[A].push_back(s);
+        rowbuf.resize(W);
+    }
+
+    // ---- lexical pass for one q: group tokens by (emitted x, end state p)
+    void lexical_pass(int32_t q, Interner<int32_t> &groups) {
+        int32_t N = (int32_t)VT.depth.size();
+        int32_t maxd = 0;
+        for (int32_t d : VT.depth) maxd = std::max(maxd, d);
+        std::vector<int32_t> cur(maxd + 2), emlen(maxd + 2), embuf(maxd + 2), key(maxd + 3);
+        cur[0] = q;
+        emlen[0] = 0;
+        grp_tokens.clear();
+        int32_t i = 1;
+        while (i < N) {
+            int32_t d = VT.depth[i];
+            uint8_t c = VT.byte[i];
+            int32_t s = cur[d - 1];
+            int32_t em = emlen[d - 1];
+            int32_t nx = G.lex_next[(int64_t)s * 256 + c];
+            if (nx < 0) {
+                int32_t t = (s != 0) ? G.lex_accept[s] : -1;
+                if (t >= 0) {
+                    if (!G.ign[t]) embuf[em++] = t;
+                    nx = G.lex_next[c];
+                }
+            }
+            if (nx < 0) {           // the lexer dies: no token below this node is valid
+                i = VT.subtree_end[i];
+                continue;
+            }
+            cur[d] = nx;
+            emlen[d] = em;
+            if (VT.tok_end[i] > VT.tok_begin[i]) {
+                key[0] = nx;
+                for (int32_t k = 0; k < em; k++) key[1 + k] = embuf[k];
+                bool added;
+                int32_t gid = groups.find_or_add(key.data(), (size_t)em + 1, &added);
+                if (added) grp_tokens.emplace_back();
+                auto &lst = grp_tokens[gid];
+                lst.insert(lst.end(), VT.toks.begin() + VT.tok_begin[i], VT.toks.begin() + VT.tok_end[i]);
+            }
+            i++;
+        }
+    }
+
+    // ---- the trie of realizable terminal sequences R_q(V) for one q
+    void sequence_trie(int32_t q, const Interner<int32_t> &groups) {
+        std::vector<int32_t> label{-1};
+        std::vector<std::unordered_map<int32_t, int32_t>> kids(1);
+        std::vector<std::vector<int32_t>> ngrps(1);
+        auto child = [&](int32_t n, int32_t t) {
+            auto it = kids[n].find(t);
+            if (it != kids[n].end()) return it->second;
+            int32_t id = (int32_t)label.size();
+            label.push_back(t);
+            kids.emplace_back();
+            ngrps.emplace_back();
+            kids[n].emplace(t, id);
+            return id;
+        };
+        int32_t n_groups = (int32_t)groups.size();
+        for (int32_t g = 0; g < n_groups; g++) {
+            const int32_t *k = groups.data(g);
+            size_t len = groups.len(g);
+            int32_t p = k[0];
+            int32_t n = 0;
+            for (size_t j = 1; j < len; j++) n = child(n, k[j]);
+            if (C.eps[p]) ngrps[n].push_back(g);
+            for (int32_t t : C.terms[p]) ngrps[child(n, t)].push_back(g);
+        }
+        // EOS: the pending lexeme must end here, then $end must be accepted
+        if (vocab->eos_id >= 0) {
+            int32_t n = -1;
+            if (q == 0) n = child(0, G.endT);
+            else if (G.lex_accept[q] >= 0) {
+                int32_t t = G.lex_accept[q];
+                n = G.ign[t] ? child(0, G.endT) : child(child(0, t), G.endT);
+            }
+            if (n >= 0) {
+                grp_tokens.push_back({vocab->eos_id});
+                ngrps[n].push_back((int32_t)grp_tokens.size() - 1);
+            }
+        }
+        int32_t N = (int32_t)label.size();
+        tn_label = label;
+        tn_child_beg.assign(N, 0);
+        tn_child_end.assign(N, 0);
+        tn_children.clear();
+        tn_grp_beg.assign(N, 0);
+        tn_grp_end.assign(N, 0);
+        tn_grps.clear();
+        for (int32_t n = 0; n < N; n++) {
+            tn_child_beg[n] = (int32_t)tn_children.size();
+            std::vector<std::pair<int32_t, int32_t>> kv(kids[n].begin(), kids[n].end());
+            std::sort(kv.begin(), kv.end());
+            for (auto &x : kv) tn_children.push_back(x.second);
+            tn_child_end[n] = (int32_t)tn_children.size();
+            tn_grp_beg[n] = (int32_t)tn_grps.size();
+            tn_grps.insert(tn_grps.end(), ngrps[n].begin(), ngrps[n].end());
+            tn_grp_end[n] = (int32_t)tn_grps.size();
+        }
+    }
+
+    // ---- parser simulation on a known stack top (beta, top at back)
+    void run(int32_t c, std::vector<int32_t> &beta) {
+        const int32_t t = tn_label[c];
+        for (;;) {
+            int32_t a = G.act(beta.back(), t);
+            switch (a & 3) {
+            case 1:                       // shift: the stack is stable again
+                beta.push_back(a >> 2);
+                visit(c, beta);
+                return;
+            case 3:                       // accept ($end)
+                acc.push_back(c);
+                return;
+            case 2: {                     // reduce
+                int32_t p = a >> 2, m = G.plen[p], A = G.plhs[p];
+                if (m < (int32_t)beta.size()) {
+                    beta.resize(beta.size() - m);
+                    int32_t g = G.gto(beta.back(), A);
+                    if (g < 0) return;
+                    beta.push_back(g);
+                    continue;
+                }
+                int32_t k = m - (int32_t)beta.size();
+                if (k > 0xFFFE) throw BuildError(PSC_E_LIMIT, "production too long");
+                newW.push_back(pack_thread(c, k, A));
+                return;
+            }
+            default:
+                return;
+            }
+        }
+    }
+
+    void visit(int32_t c, const std::vector<int32_t> &beta) {
+        if (tn_grp_end[c] > tn_grp_beg[c]) acc.push_back(c);
+        for (int32_t j = tn_child_beg[c]; j < tn_child_end[c]; j++) {
+            std::vector<int32_t> b2 = beta;
+            run(tn_children[j], b2);
+        }
+    }
+
+    // mask class after accepting every token of trie node c
+    int32_t add_node(int32_t cls, int32_t c) {
+        uint64_t key = ((uint64_t)(uint32_t)cls << 32) | (uint32_t)c;
+        auto it = add_memo.find(key);
+        if (it != add_memo.end()) return it->second;
+        const uint32_t *src = masks.data(cls);
+        std::copy(src, src + W, rowbuf.begin());
+        for (int32_t j = tn_grp_beg[c]; j < tn_grp_end[c]; j++)
+            for (int32_t tok : grp_tokens[tn_grps[j]]) rowbuf[tok >> 5] |= 1u << (tok & 31);
+        bool added;
+        int32_t out = masks.find_or_add(rowbuf.data(), W, &added);
+        add_memo.emplace(key, out);
+        return out;
+    }
+
+    int32_t new_global_state(int32_t cls) {
+        int32_t id = (int32_t)st_cls.size();
+        st_cls.push_back(cls);
+        st_def.push_back(id);
+        st_ebeg.push_back(0);
+        st_eend.push_back(0);
+        states_built++;
+        if (states_built > 40'000'000) throw BuildError(PSC_E_LIMIT, "automaton exceeds 40M states");
+        return id;
+    }
+
+    // state id for (threads, cls); queue new per-q states
+    int32_t intern(std::vector<uint64_t> &th, int32_t cls, std::vector<int32_t> &queue) {
+        std::sort(th.begin(), th.end());
+        th.erase(std::unique(th.begin(), th.end()), th.end());
+        if (th.empty()) {
+            auto it = empty_state_of_cls.find(cls);
+            if (it != empty_state_of_cls.end()) return it->second;
+            int32_t id = new_global_state(cls);   // absorbing: default is itself
+            empty_state_of_cls.emplace(cls, id);
+            return id;
+        }
+        std::vector<uint64_t> key;
+        key.reserve(th.size() + 1);
+        key.push_back((uint64_t)(uint32_t)cls);
+        key.insert(key.end(), th.begin(), th.end());
+        bool added;
+        int32_t qid = qstates.find_or_add(key.data(), key.size(), &added);
+        if (added) {
+            qstate_global.push_back(new_global_state(cls));
+            queue.push_back(qid);
+        }
+        return qstate_global[qid];
+    }
+
+    int32_t step(const uint64_t *th, size_t n, int32_t cls, int32_t X, std::vector<int32_t> &queue) {
+        newW.clear();
+        acc.clear();
+        std::vector<int32_t> beta;
+        for (size_t i = 0; i < n; i++) {
+            uint64_t t = th[i];
+            int32_t c = th_node(t), k = th_k(t), A = th_A(t);
+            if (A == kInitA) {
+                for (int32_t j = tn_child_beg[c]; j < tn_child_end[c]; j++) {
+                    beta.assign(1, X);
+                    run(tn_children[j], beta);
+                }
+            } else if (k > 0) {
+                newW.push_back(pack_thread(c, k - 1, A));
+            } else {
+                int32_t g = G.gto(X, A);
+                if (g < 0) continue;
+                beta.assign({X, g});
+                run(c, beta);
+            }
+        }
+        std::sort(acc.begin(), acc.end());
+        acc.erase(std::unique(acc.begin(), acc.end()), acc.end());
+        int32_t cls2 = cls;
+        for (int32_t c : acc) cls2 = add_node(cls2, c);
+        std::vector<uint64_t> w2 = newW;
+        return intern(w2, cls2, queue);
+    }
+
+    void build_for_lexer_state(int32_t q) {
+        Interner<int32_t> groups;
+        lexical_pass(q, groups);
+        sequence_trie(q, groups);
+        qstates.clear();
+        qstate_global.clear();
+        add_memo.clear();
+        std::vector<int32_t> queue;
+        int32_t cls0 = 0;
+        if (tn_grp_end[0] > tn_grp_beg[0]) cls0 = add_node(0, 0);
+        std::vector<uint64_t> init{pack_thread(0, 0, kInitA)};
+        start_state[q] = intern(init, cls0, queue);
+        std::vector<uint64_t> key, dW;
+        std::vector<int32_t> syms;
+        std::vector<uint8_t> seen(G.nPi, 0);
+        for (size_t qi = 0; qi < queue.size(); qi++) {
+            int32_t qid = queue[qi];
+            key.assign(qstates.data(qid), qstates.data(qid) + qstates.len(qid));
+            int32_t gid = qstate_global[qid];
+            int32_t cls = (int32_t)key[0];
+            const uint64_t *th = key.data() + 1;
+            size_t n = key.size() - 1;
+            // default transition: waiting-to-skip threads advance, others die
+            dW.clear();
+            bool init = false;
+            syms.clear();
+            for (size_t i = 0; i < n; i++) {
+                int32_t k = th_k(th[i]), A = th_A(th[i]);
+                if (A == kInitA) init = true;
+                else if (k > 0) dW.push_back(pack_thread(th_node(th[i]), k - 1, A));
+                else
+                    for (int32_t X : goto_sources[A])
+                        if (!seen[X]) { seen[X] = 1; syms.push_back(X); }
+            }
+            if (init) {
+                for (int32_t X : syms) seen[X] = 0;
+                syms.clear();
+                for (int32_t X = 0; X < G.nPi; X++) syms.push_back(X);
+            } else {
+                for (int32_t X : syms) seen[X] = 0;
+            }
+            std::sort(syms.begin(), syms.end());
+            int32_t def = intern(dW, cls, queue);
+            int32_t ebeg = (int32_t)e_sym.size();
+            for (int32_t X : syms) {
+                int32_t tgt = step(th, n, cls, X, queue);
+                if (tgt != def) {
+                    e_sym.push_back(X);
+                    e_tgt.push_back(tgt);
+                }
+            }
+            st_def[gid] = def;
+            st_ebeg[gid] = ebeg;
+            st_eend[gid] = (int32_t)e_sym.size();
+        }
+        if (verbose)
+            std::fprintf(stderr, "psc_build: q=%d groups=%zu trie=%zu states=%zu (total %lld) classes=%zu\n", q,
+                         groups.size(), tn_label.size(), queue.size(), (long long)states_built, masks.size());
+    }
+};
+
+// ---------------------------------------------------------- minimisation
+
+// Moore refinement over total transition functions (default + explicit
+// edges); block 0..n-1 ids returned per state.
+std::vector<int32_t> minimise(const Builder &B, int32_t *n_blocks_out) {
+    int32_t N = (int32_t)B.st_cls.size();
+    std::vector<int32_t> block(N);
+    {
+        Interner<int32_t> in;
+        for (int32_t s = 0; s < N; s++) {
+            bool a;
+            block[s] = in.find_or_add(&B.st_cls[s], 1, &a);
+        }
+    }
+    int32_t nb = 0;
+    for (int32_t b : block) nb = std::max(nb, b + 1);
+    std::vector<int32_t> sig;
+    while (true) {
+        Interner<int32_t> in;
+        std::vector<int32_t> nbk(N);
+        for (int32_t s = 0; s < N; s++) {
+            sig.clear();
+            int32_t db = block[B.st_def[s]];
+            sig.push_back(block[s]);
+            sig.push_back(db);
+            for (int32_t e = B.st_ebeg[s]; e < B.st_eend[s]; e++) {
+                int32_t tb = block[B.e_tgt[e]];
+                if (tb != db) { sig.push_back(B.e_sym[e]); sig.push_back(tb); }
+            }
+            bool a;
+            nbk[s] = in.find_or_add(sig.data(), sig.size(), &a);
+        }
+        int32_t nnb = (int32_t)in.size();
+        block.swap(nbk);
+        if (nnb == nb) break;
+        nb = nnb;
+    }
+    *n_blocks_out = nb;
+    return block;
+}
+
+}  // namespace
+}  // namespace psc
+
+using namespace psc;
+
+size_t psc_handle::device_bytes_needed() const {
+    size_t tb = (table.size() * sizeof(int32_t) + 255) & ~(size_t)255;
+    return kTableOff + tb + masks.size() * sizeof(uint32_t);
+}
+
+extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out) {
+    auto t0 = std::chrono::steady_clock::now();
+    if (!grammar || !vocab || !out) {
+        set_error("psc_build: null argument");
+        return PSC_E_INVALID_ARG;
+    }
+    *out = nullptr;
+    try {
+        validate(grammar, vocab);
+        Gram G{grammar->n_lex_states, grammar->n_terminals, grammar->n_lr_states, grammar->n_nonterminals,
+               grammar->n_productions, grammar->end_terminal, grammar->lex_next, grammar->lex_accept,
+               grammar->action, grammar->goto_table, grammar->prod_lhs, grammar->prod_len,
+               grammar->terminal_ignored};
+        bool verbose = std::getenv("PSC_BUILD_VERBOSE") != nullptr;
+        Completions C = completions(G);
+        VocabTrie VT = vocab_trie(vocab);
+        Builder B(G, vocab, C, VT, verbose);
+        B.start_state.assign(G.nQ, -1);
+        for (int32_t q = 0; q < G.nQ; q++) B.build_for_lexer_state(q);
+
+        int32_t nb = 0;
+        std::vector<int32_t> block = minimise(B, &nb);
+        int32_t N = (int32_t)B.st_cls.size();
+        std::vector<int32_t> rep(nb, -1);
+        for (int32_t s = 0; s < N; s++)
+            if (rep[block[s]] < 0) rep[block[s]] = s;
+
+        // minimised automaton: per block, end class, default block, edges
+        std::vector<int32_t> m_cls(nb), m_def(nb), m_ebeg(nb + 1);
+        std::vector<int32_t> m_sym, m_tgt;
+        for (int32_t b = 0; b < nb; b++) {
+            int32_t s = rep[b];
+            m_cls[b] = B.st_cls[s];
+            m_def[b] = block[B.st_def[s]];
+            m_ebeg[b] = (int32_t)m_sym.size();
+            for (int32_t e = B.st_ebeg[s]; e < B.st_eend[s]; e++) {
+                int32_t tb = block[B.e_tgt[e]];
+                if (tb != m_def[b]) { m_sym.push_back(B.e_sym[e]); m_tgt.push_back(tb); }
+            }
+        }
+        m_ebeg[nb] = (int32_t)m_sym.size();
+
+        // determined(b): every state reachable from b has the same class.
+        // Tarjan's SCCs come out successors-first, so one pass suffices.
+        const int32_t MANY = -2, UNSET = -3;
+        std::vector<int32_t> det(nb, UNSET), idx(nb, -1), low(nb, 0), comp_stack;
+        std::vector<uint8_t> on(nb, 0), in_comp(nb, 0);
+        int32_t counter = 0;
+        auto succ_count = [&](int32_t b) { return 1 + (m_ebeg[b + 1] - m_ebeg[b]); };
+        auto succ_at = [&](int32_t b, int32_t i) { return i == 0 ? m_def[b] : m_tgt[m_ebeg[b] + i - 1]; };
+        for (int32_t root = 0; root < nb; root++) {
+            if (idx[root] >= 0) continue;
+            std::vector<std::pair<int32_t, int32_t>> work{{root, 0}};
+            while (!work.empty()) {
+                auto &[v, it] = work.back();
+                if (it == 0 && idx[v] < 0) {
+                    idx[v] = low[v] = counter++;
+                    comp_stack.push_back(v);
+                    on[v] = 1;
+                }
+                bool descended = false;
+                while (it < succ_count(v)) {
+                    int32_t w = succ_at(v, it);
+                    it++;
+                    if (idx[w] < 0) {
+                        work.emplace_back(w, 0);
+                        descended = true;
+                        break;
+                    }
+                    if (on[w]) low[v] = std::min(low[v], idx[w]);
+                }
+                if (descended) continue;
+                int32_t vv = v;
+                if (low[vv] == idx[vv]) {
+                    std::vector<int32_t> members;
+                    while (true) {
+                        int32_t x = comp_stack.back();
+                        comp_stack.pop_back();
+                        on[x] = 0;
+                        members.push_back(x);
+                        if (x == vv) break;
+                    }
+                    int32_t d = m_cls[members[0]];
+                    for (int32_t x : members) in_comp[x] = 1;
+                    for (int32_t x : members) {
+                        if (m_cls[x] != d) d = MANY;
+                        for (int32_t i = 0; i < succ_count(x) && d != MANY; i++) {
+                            int32_t w = succ_at(x, i);
+                            if (!in_comp[w] && det[w] != d) d = MANY;
+                        }
+                    }
+                    for (int32_t x : members) { det[x] = d; in_comp[x] = 0; }
+                }
+                work.pop_back();
+                if (!work.empty()) {
+                    int32_t parent = work.back().first;
+                    low[parent] = std::min(low[parent], low[vv]);
+                }
+            }
+        }
+
+        // keep only the classes a walk can end in, renumbered densely
+        // (class 0, the all-zero row, always keeps id 0)
+        std::vector<int32_t> cls_map(B.masks.size(), -1);
+        std::vector<int32_t> kept{0};
+        cls_map[0] = 0;
+        auto keep = [&](int32_t c) {
+            if (cls_map[c] < 0) { cls_map[c] = (int32_t)kept.size(); kept.push_back(c); }
+            return cls_map[c];
+        };
+        for (int32_t b = 0; b < nb; b++) {
+            m_cls[b] = keep(m_cls[b]);
+            if (det[b] >= 0) det[b] = keep(det[b]);
+        }
+
+        // flatten
+        psc_handle *h = new psc_handle();
+        h->V = vocab->n_tokens;
+        h->W = (vocab->n_tokens + 31) / 32;
+        h->mask_stride = (h->W + 63) & ~63;   // 256-byte rows
+        h->n_lex = G.nQ;
+        h->n_lr = G.nPi;
+        h->n_classes = (int32_t)kept.size();
+        std::vector<int32_t> ref(nb, 0);
+        int64_t off = G.nQ + (G.nQ & 1);
+        int32_t rows = 0, dense = 0, max_sparse = 0;
+        for (int32_t b = 0; b < nb; b++) {
+            if (det[b] >= 0) { ref[b] = class_ref(det[b]); continue; }
+            int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
+            bool is_dense = ne > kSparseMax;
+            ref[b] = (int32_t)off | (is_dense ? 1 : 0);
+            int64_t len = kRowHeader + (is_dense ? (int64_t)G.nPi : 2LL * ne);
+            off += len + (len & 1);
+            rows++;
+            if (is_dense) dense++; else max_sparse = std::max(max_sparse, ne);
+            if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
+        }
+        h->table.assign((size_t)off + kTablePad, 0);
+        for (int32_t q = 0; q < G.nQ; q++) h->table[q] = ref[block[B.start_state[q]]];
+        for (int32_t b = 0; b < nb; b++) {
+            if (det[b] >= 0) continue;
+            int32_t *row = h->table.data() + ref_offset(ref[b]);
+            int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
+            row[0] = m_cls[b];
+            row[3] = 0;
+            if (ref_is_dense(ref[b])) {
+                row[1] = -1;
+                row[2] = ref[m_def[b]];
+                for (int32_t X = 0; X < G.nPi; X++) row[kRowHeader + X] = ref[m_def[b]];
+                for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) row[kRowHeader + m_sym[e]] = ref[m_tgt[e]];
+            } else {
+                row[1] = ne;
+                row[2] = ref[m_def[b]];
+                for (int32_t e = 0; e < ne; e++) {
+                    row[kRowHeader + 2 * e] = m_sym[m_ebeg[b] + e];
+                    row[kRowHeader + 2 * e + 1] = ref[m_tgt[m_ebeg[b] + e]];
+                }
+            }
+        }
+        h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);
+        for (int32_t c = 0; c < h->n_classes; c++)
+            std::copy(B.masks.data(kept[c]), B.masks.data(kept[c]) + h->W,
+                      h->masks.begin() + (size_t)c * h->mask_stride);
+
+        psc_info_t &I = h->info;
+        I.vocab_size = h->V;
+        I.mask_words = h->W;
+        I.mask_stride_words = h->mask_stride;
+        I.n_lex_states = G.nQ;
+        I.n_lr_states = G.nPi;
+        I.n_classes = h->n_classes;
+        I.dfa_states_built = B.states_built;
+        I.dfa_states = nb;
+        I.dfa_rows = rows;
+        I.dense_rows = dense;
+        I.max_sparse_edges = max_sparse;
+        I.table_bytes = (int64_t)h->table.size() * 4;
+        I.mask_table_bytes = (int64_t)h->masks.size() * 4;
+        I.device_bytes = (int64_t)h->device_bytes_needed();
+        I.build_seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+        *out = h;
+        return PSC_OK;
+    } catch (const BuildError &e) {
+        set_error(std::string("psc_build: ") + e.what());
+        return e.code;
+    } catch (const std::bad_alloc &) {
+        set_error("psc_build: out of host memory");
+        return PSC_E_OOM;
+    }
+}
+
+extern "C" psc_status psc_info(const psc_handle *h, psc_info_t *out) {
+    if (!h || !out) {
+        set_error("psc_info: null argument");
+        return PSC_E_INVALID_ARG;
+    }
+    *out = h->info;
+    return PSC_OK;
+}
+
+extern "C" size_t psc_device_bytes(const psc_handle *h) { return h ? h->device_bytes_needed() : 0; }
+
+extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                        const int32_t *lexer_states, int32_t B, int32_t *out_classes) {
+    if (!h || B < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_classes))) {
+        set_error("psc_classify_host: invalid argument");
+        return PSC_E_INVALID_ARG;
+    }
+    const int32_t *T = h->table.data();
+    int64_t base = 0;
+    for (int32_t b = 0; b < B; b++) {
+        int32_t len = stack_lens[b], q = lexer_states[b];
+        const int32_t *st = stacks + base;
+        base += len > 0 ? len : 0;
+        if (len <= 0 || q < 0 || q >= h->n_lex) { out_classes[b] = -1; continue; }
+        int32_t ref = T[q];
+        int32_t i = len - 1;
+        int32_t cls = -1;
+        for (;;) {
+            if (ref_is_class(ref)) { cls = ref_class(ref); break; }
+            const int32_t *row = T + ref_offset(ref);
+            if (i < 0) { cls = row[0]; break; }
+            int32_t X = st[i--];
+            if (X < 0 || X >= h->n_lr) { cls = -1; break; }
+            if (ref_is_dense(ref)) {
+                ref = row[kRowHeader + X];
+            } else {
+                int32_t lo = 0, hi = row[1], nxt = row[2];
+                while (lo < hi) {
+                    int32_t mid = (lo + hi) / 2, s = row[kRowHeader + 2 * mid];
+                    if (s == X) { nxt = row[kRowHeader + 2 * mid + 1]; break; }
+                    if (s < X) lo = mid + 1; else hi = mid;
+                }
+                ref = nxt;
+            }
+        }
+        out_classes[b] = cls;
+    }
+    return PSC_OK;
+}
+
+extern "C" psc_status psc_class_mask_host(const psc_handle *h, int32_t cls, uint32_t *out_row) {
+    if (!h || !out_row || cls < 0 || cls >= h->n_classes) {
+        set_error("psc_class_mask_host: invalid argument");
+        return PSC_E_INVALID_ARG;
+    }
+    std::copy(h->masks.begin() + (size_t)cls * h->mask_stride,
+              h->masks.begin() + (size_t)cls * h->mask_stride + h->W, out_row);
+    return PSC_OK;
+}
+
+extern "C" void psc_free(psc_handle *h) { delete h; }
+
+extern "C" const char *psc_last_error(void) { return g_last_error.c_str(); }

@@ -1,0 +1,220 @@
+"""Python binding of libpsc.so (include/psc.h): argument marshalling only.
+
+Every step of the mask path runs in the library's HIP kernels; torch is used
+for device memory and streams.  There is no fallback: if the library is
+missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpsc.so")
+
+PSC_F32, PSC_BF16 = 0, 1
+_STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E_OOM",
+           -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT"}
+
+EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
+            "psc_apply_mask", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_free", "psc_last_error"]
+
+
+class PscError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class _Grammar(C.Structure):
+    _fields_ = [
+        ("n_lex_states", C.c_int32), ("lex_next", C.c_void_p), ("lex_accept", C.c_void_p),
+        ("n_terminals", C.c_int32), ("terminal_ignored", C.c_void_p), ("end_terminal", C.c_int32),
+        ("n_lr_states", C.c_int32), ("n_nonterminals", C.c_int32), ("action", C.c_void_p),
+        ("goto_table", C.c_void_p), ("n_productions", C.c_int32), ("prod_lhs", C.c_void_p),
+        ("prod_len", C.c_void_p),
+    ]
+
+
+class _Vocab(C.Structure):
+    _fields_ = [("n_tokens", C.c_int32), ("bytes", C.c_void_p), ("offsets", C.c_void_p),
+                ("eos_id", C.c_int32)]
+
+
+class Info(C.Structure):
+    _fields_ = [
+        ("vocab_size", C.c_int32), ("mask_words", C.c_int32), ("mask_stride_words", C.c_int32),
+        ("n_lex_states", C.c_int32), ("n_lr_states", C.c_int32), ("n_classes", C.c_int32),
+        ("dfa_states_built", C.c_int64), ("dfa_states", C.c_int32), ("dfa_rows", C.c_int32),
+        ("dense_rows", C.c_int32), ("max_sparse_edges", C.c_int32), ("table_bytes", C.c_int64),
+        ("mask_table_bytes", C.c_int64), ("device_bytes", C.c_int64), ("build_seconds", C.c_double),
+    ]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load libpsc.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() "
+                              "(or python paper_2608_03065_amd/build.py) first")
+        L = C.CDLL(LIB_PATH)
+        P, I32, I64 = C.c_void_p, C.c_int32, C.c_int64
+        L.psc_build.argtypes = [P, P, C.POINTER(P)]
+        L.psc_info.argtypes = [P, P]
+        L.psc_device_bytes.argtypes = [P]
+        L.psc_device_bytes.restype = C.c_size_t
+        L.psc_bind_device.argtypes = [P, P, C.c_size_t, P]
+        L.psc_compute_masks.argtypes = [P, P, P, P, I32, P, P]
+        L.psc_apply_mask.argtypes = [P, C.c_int, P, I32, I32, P]
+        L.psc_device_error_count.argtypes = [P, P, I32, P]
+        L.psc_classify_host.argtypes = [P, P, P, P, I32, P]
+        L.psc_class_mask_host.argtypes = [P, I32, P]
+        L.psc_free.argtypes = [P]
+        L.psc_free.restype = None
+        L.psc_last_error.restype = C.c_char_p
+        for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
+                     "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
+            getattr(L, name).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise PscError(status, lib().psc_last_error().decode(errors="replace"))
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def pack_states(states, device=None):
+    """[(q, stack bottom->top), ...] -> (stacks int32 [sum len], lens int32 [B], qs int32 [B]),
+    numpy on the host, or torch tensors on `device` when given."""
+    lens = np.array([len(s[1]) for s in states], dtype=np.int32)
+    qs = np.array([s[0] for s in states], dtype=np.int32)
+    stacks = (np.concatenate([np.asarray(s[1], dtype=np.int32) for s in states])
+              if len(states) else np.zeros(0, np.int32))
+    if device is None:
+        return stacks, lens, qs
+    import torch
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    return t(stacks if stacks.size else np.zeros(1, np.int32)), t(lens), t(qs)
+
+
+class Classifier:
+    """A built (grammar, vocabulary) classifier: psc_build .. psc_free."""
+
+    def __init__(self, grammar, vocab):
+        g = grammar
+        arrs = dict(
+            lex_next=np.ascontiguousarray(g.lexer.next, dtype=np.int32),
+            lex_accept=np.ascontiguousarray(g.lexer.accept, dtype=np.int32),
+            ignored=np.ascontiguousarray(g.terminal_ignored, dtype=np.uint8),
+            action=np.ascontiguousarray(g.action, dtype=np.int32),
+            goto=np.ascontiguousarray(g.goto, dtype=np.int32),
+            lhs=np.ascontiguousarray(g.prod_lhs, dtype=np.int32),
+            plen=np.ascontiguousarray(g.prod_len, dtype=np.int32),
+        )
+        toks = vocab.tokens
+        offs = np.zeros(len(toks) + 1, dtype=np.int64)
+        np.cumsum([len(t) for t in toks], out=offs[1:])
+        blob = np.frombuffer(b"".join(toks) + b"\0", dtype=np.uint8).copy()
+        gs = _Grammar(arrs["lex_next"].shape[0], arrs["lex_next"].ctypes.data, arrs["lex_accept"].ctypes.data,
+                      arrs["action"].shape[1], arrs["ignored"].ctypes.data, int(g.end_terminal),
+                      arrs["action"].shape[0], arrs["goto"].shape[1], arrs["action"].ctypes.data,
+                      arrs["goto"].ctypes.data, arrs["lhs"].shape[0], arrs["lhs"].ctypes.data,
+                      arrs["plen"].ctypes.data)
+        vs = _Vocab(len(toks), blob.ctypes.data, offs.ctypes.data, int(vocab.eos_id))
+        h = C.c_void_p()
+        _check(lib().psc_build(C.addressof(gs), C.addressof(vs), C.byref(h)))
+        self._h = h
+        self._dev = None
+        self.V = len(toks)
+        self.W = (self.V + 31) // 32
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            _lib.psc_free(self._h)
+            self._h = None
+
+    # ---------------------------------------------------------------- host
+    def info(self) -> dict:
+        inf = Info()
+        _check(lib().psc_info(self._h, C.byref(inf)))
+        return inf.as_dict()
+
+    def classify_host(self, states) -> np.ndarray:
+        stacks, lens, qs = pack_states(states)
+        out = np.zeros(len(states), np.int32)
+        st = stacks if stacks.size else np.zeros(1, np.int32)
+        _check(lib().psc_classify_host(self._h, st.ctypes.data, lens.ctypes.data, qs.ctypes.data,
+                                       len(states), out.ctypes.data))
+        return out
+
+    def class_mask(self, cls: int) -> np.ndarray:
+        row = np.zeros(self.W, np.uint32)
+        _check(lib().psc_class_mask_host(self._h, int(cls), row.ctypes.data))
+        return row
+
+    def masks_host(self, states) -> np.ndarray:
+        """Host walk + mask lookup (triage; not a device path)."""
+        cls = self.classify_host(states)
+        out = np.zeros((len(states), self.W), np.uint32)
+        for i, c in enumerate(cls):
+            if c >= 0:
+                out[i] = self.class_mask(c)
+        return out
+
+    # -------------------------------------------------------------- device
+    def bind(self, device="cuda", stream=None):
+        import torch
+        n = int(lib().psc_device_bytes(self._h))
+        buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
+        off = (-buf.data_ptr()) % 256
+        self._dev = buf
+        self._dev_ptr = buf.data_ptr() + off
+        _check(lib().psc_bind_device(self._h, self._dev_ptr, n, _stream_ptr(stream)))
+        return self
+
+    def compute_masks(self, stacks, stack_lens, lexer_states, out=None, stream=None):
+        """Device int32 tensors -> uint32 bitmask [B, W] (torch.int32 view)."""
+        import torch
+        B = int(stack_lens.shape[0])
+        for t in (stacks, stack_lens, lexer_states):
+            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
+        if out is None:
+            out = torch.empty((B, self.W), dtype=torch.int32, device=stack_lens.device)
+        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and tuple(out.shape) == (B, self.W)
+        _check(lib().psc_compute_masks(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
+                                       lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
+        return out
+
+    def error_count(self, reset: bool = False, stream=None) -> int:
+        v = C.c_uint32()
+        _check(lib().psc_device_error_count(self._h, C.byref(v), int(reset), _stream_ptr(stream)))
+        return int(v.value)
+
+
+def apply_mask(logits, bitmask, stream=None):
+    """In place: logits[b, v] = -inf where bit v of bitmask[b] is 0."""
+    import torch
+    assert logits.is_cuda and logits.is_contiguous() and logits.dim() == 2
+    B, V = logits.shape
+    assert bitmask.is_cuda and bitmask.is_contiguous() and tuple(bitmask.shape) == (B, (V + 31) // 32)
+    dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+    _check(lib().psc_apply_mask(logits.data_ptr(), dt, bitmask.data_ptr(), B, V, _stream_ptr(stream)))
+    return logits

@@ -1,0 +1,132 @@
+"""CPU checks of the library: exports, argument errors, and the host walk of
+the built classifier against the oracle (bit-exact)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from inputs import configs
+from inputs.vocab import Vocab
+from oracle import Oracle
+from paper_2608_03065_amd import psc
+from paper_2608_03065_amd.psc import Classifier, PscError
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "psc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(psc_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 10
+    lib = psc.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(psc.EXPORTED) == names
+
+
+@pytest.mark.parametrize("name,steps", [("arithmetic", 200), ("json", 40)])
+def test_host_walk_matches_oracle(name, steps):
+    wl = configs.get(name)
+    clf = Classifier(wl.grammar, wl.vocab)
+    states = [st for s in range(steps) for st in wl.states(s)]
+    got = clf.masks_host(states)
+    want = Oracle(wl.grammar, wl.vocab).masks(states)
+    bad = np.nonzero((got != want).any(axis=1))[0]
+    assert bad.size == 0, f"{bad.size} rows differ, first at {bad[:5]}"
+
+
+def test_classes_partition_is_consistent_with_oracle():
+    # rows that share a class must have identical oracle rows
+    wl = configs.get("json")
+    clf = Classifier(wl.grammar, wl.vocab)
+    states = [st for s in range(40, 60) for st in wl.states(s)]
+    cls = clf.classify_host(states)
+    want = Oracle(wl.grammar, wl.vocab).masks(states)
+    for c in np.unique(cls):
+        rows = want[cls == c]
+        assert (rows == rows[0]).all()
+
+
+def test_info_is_consistent():
+    wl = configs.get("json")
+    inf = Classifier(wl.grammar, wl.vocab).info()
+    assert inf["vocab_size"] == wl.V and inf["mask_words"] == (wl.V + 31) // 32
+    assert inf["mask_stride_words"] % 64 == 0 and inf["mask_stride_words"] >= inf["mask_words"]
+    assert inf["dfa_states"] <= inf["dfa_states_built"]
+    assert inf["device_bytes"] >= inf["table_bytes"] + inf["mask_table_bytes"]
+
+
+def test_host_walk_range_faults():
+    wl = configs.get("arithmetic")
+    clf = Classifier(wl.grammar, wl.vocab)
+    good = wl.states(0)[0]
+    n_lex = wl.grammar.lexer.n_states
+    bad_q = (n_lex, good[1])
+    bad_sym = (good[0], np.array([0, wl.grammar.n_lr_states + 5], np.int32))
+    cls = clf.classify_host([good, bad_q, bad_sym])
+    assert cls[0] >= 0 and cls[1] == -1 and cls[2] == -1
+
+
+def _tables(wl):
+    return wl.grammar
+
+
+def test_build_rejects_bad_inputs():
+    wl = configs.get("arithmetic")
+    g = wl.grammar
+    # EOS with a spelling
+    v = Vocab([b"1", b"+", b"x"], 2)
+    with pytest.raises(PscError) as e:
+        Classifier(g, v)
+    assert e.value.status == -2
+    # a non-EOS token with an empty spelling
+    v = Vocab([b"1", b"", b""], 2)
+    with pytest.raises(PscError) as e:
+        Classifier(g, v)
+    assert e.value.status == -2
+
+    class Broken:
+        pass
+    b = Broken()
+    b.lexer = type("L", (), {})()
+    b.lexer.next = g.lexer.next.copy()
+    b.lexer.accept = g.lexer.accept.copy()
+    b.lexer.accept[0] = 1                  # q0 accepting is not allowed
+    for k in ("terminal_ignored", "end_terminal", "action", "goto", "prod_lhs", "prod_len"):
+        setattr(b, k, getattr(g, k))
+    with pytest.raises(PscError) as e:
+        Classifier(b, wl.vocab)
+    assert e.value.status == -2
+    b.lexer.accept = g.lexer.accept
+    b.action = g.action.copy()
+    b.action[0, 0] = (999 << 2) | 1        # shift target out of range
+    with pytest.raises(PscError) as e:
+        Classifier(b, wl.vocab)
+    assert e.value.status == -2
+
+
+def test_null_arguments():
+    lib = psc.lib()
+    h = C.c_void_p()
+    assert lib.psc_build(None, None, C.byref(h)) == -1
+    assert lib.psc_info(None, None) == -1
+    assert lib.psc_compute_masks(None, None, None, None, 1, None, None) == -1
+    assert lib.psc_apply_mask(None, 0, None, -1, 5, None) == -1
+    assert lib.psc_apply_mask(None, 7, None, 1, 5, None) == -1
+    assert lib.psc_apply_mask(None, 0, None, 0, 5, None) == 0      # B == 0: no-op
+    assert b"null" in lib.psc_last_error() or lib.psc_last_error()
+
+
+def test_compute_masks_requires_binding():
+    wl = configs.get("arithmetic")
+    clf = Classifier(wl.grammar, wl.vocab)
+    dummy = C.c_int32(0)
+    st = psc.lib().psc_compute_masks(clf._h, C.addressof(dummy), C.addressof(dummy), C.addressof(dummy), 1,
+                                     C.addressof(dummy), None)
+    assert st == -6
