@@ -13,7 +13,7 @@ from typing import Callable
 
 import numpy as np
 
-from . import documents, grammars, vocab
+from . import documents, grammars, schema, vocab
 from .grammar import GrammarTables
 from .native import HostParser
 from .seeds import rng_for
@@ -31,6 +31,7 @@ class Workload:
     make_vocab: Callable[[GrammarTables], vocab.Vocab]
     make_document: Callable[[np.random.Generator, "Workload"], bytes]
     description: str = ""
+    doc_pool: int = 0            # > 0: prefixes cut from a seeded pool of this many documents
 
     # ---- cached pieces ----
     @functools.cached_property
@@ -49,9 +50,18 @@ class Workload:
     def V(self) -> int:
         return self.vocab.size
 
+    @functools.cached_property
+    def documents(self) -> list[bytes]:
+        """The seeded document pool (only when doc_pool > 0)."""
+        return [self.make_document(rng_for(self.index, 0, i, salt=0xD0C5), self)
+                for i in range(self.doc_pool)]
+
     def prefix(self, step: int, b: int) -> bytes:
         rng = rng_for(self.index, step, b)
-        doc = self.make_document(rng, self)
+        if self.doc_pool:
+            doc = self.documents[int(rng.integers(0, self.doc_pool))]
+        else:
+            doc = self.make_document(rng, self)
         cut = int(rng.integers(0, len(doc) + 1))
         return doc[:cut]
 
@@ -107,6 +117,25 @@ JSON = _register(Workload(
     1, "json", B=16, steps=500, logits_dtype="f32", logits_std=1.0,
     make_grammar=grammars.json_grammar, make_vocab=_c2_vocab, make_document=_json_doc,
     description="JSON; byte-level V=32,000; B=16; fp32 N(0,1)"))
+
+
+def _c3_grammar():
+    return schema.schema_grammar(schema.c3_schema())
+
+
+def _c3_vocab(g):
+    return schema.schema_vocab(rng_for(2, salt=0x70C), schema.c3_schema(), 151936)
+
+
+def _c3_doc(rng, wl):
+    return schema.document(rng, schema.c3_schema())
+
+
+SCHEMA = _register(Workload(
+    2, "schema", B=64, steps=1000, logits_dtype="bf16", logits_std=2.0,
+    make_grammar=_c3_grammar, make_vocab=_c3_vocab, make_document=_c3_doc, doc_pool=4096,
+    description="schema-conformant JSON (seeded schema: 10 object types, 5 levels); "
+                "V=151,936; B=64; bf16 N(0,2)"))
 
 
 def get(name: str) -> Workload:

@@ -53,25 +53,25 @@ class Schema:
 
 
 def random_schema(rng: np.random.Generator, lexicon: list[bytes]) -> Schema:
-    depth = int(rng.integers(3, 6))        # levels of nested objects
+    """Nested objects: the deepest branch has 5 levels, every other nested
+    branch draws its depth from 3..5; objects above their branch's depth
+    nest 1-2 of their fields."""
     objects: dict[str, ObjType] = {}
     words = [w.decode() for w in lexicon]
 
-    def make(level: int, must_nest: bool) -> str:
+    def make(level: int, depth: int) -> str:
         name = f"o{len(objects)}"
         obj = ObjType(name)
         objects[name] = obj
         n = int(rng.integers(4, 13))
         keys = [words[i] for i in rng.choice(len(words), size=n, replace=False)]
-        n_nest = 0
-        if level < depth:
-            n_nest = int(rng.integers(1, 3))
-        nest_at = set(rng.choice(n, size=min(n_nest, n), replace=False).tolist())
-        forced = must_nest and level < depth
+        n_nest = int(rng.integers(1, 3)) if level < depth else 0
+        nest_at = sorted(rng.choice(n, size=min(n_nest, n), replace=False).tolist())
         for i, k in enumerate(keys):
             if i in nest_at:
-                child = make(level + 1, forced)
-                forced = False
+                # the first nested field continues this branch's depth
+                d = depth if i == nest_at[0] else max(level + 1, int(rng.integers(3, 6)))
+                child = make(level + 1, min(d, depth))
                 kind = "object" if rng.random() < 0.5 else "array"
                 obj.fields.append((k, kind, child))
             else:
@@ -90,7 +90,7 @@ def random_schema(rng: np.random.Generator, lexicon: list[bytes]) -> Schema:
                     obj.fields.append((k, "enum", vals))
         return name
 
-    root = make(1, True)
+    root = make(1, 5)
     return Schema(root, objects, words)
 
 
@@ -100,7 +100,7 @@ def schema_grammar(s: Schema) -> GrammarTables:
     g.regex("INT", INT)
     g.regex("FLOAT", FLOAT)
     g.ignore("WS", JSON_WS)
-    q = lambda w: '"\\"' + w + '\\""'      # a quoted literal terminal
+    q = lambda w: g.literal('"' + w + '"')   # a quoted literal terminal
     used_enum: dict[tuple, str] = {}
     for name, o in s.objects.items():
         for j, (k, kind, arg) in enumerate(o.fields):

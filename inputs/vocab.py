@@ -98,12 +98,18 @@ def piece_vocab(rng: np.random.Generator, V: int, pieces: list[bytes], weights,
     w = w / w.sum()
     n_extra = V - 1 - 256
     lengths = iter(zipf_lengths(rng, 4 * n_extra + 1000, zipf_s, lo, hi).tolist())
+    stream: list[int] = []
+
+    def draw() -> int:
+        if not stream:
+            stream.extend(rng.choice(len(pieces), size=1 << 16, p=w).tolist()[::-1])
+        return stream.pop()
 
     def one(r):
         L = next(lengths)
         buf = bytearray()
         while len(buf) < L:
-            buf += pieces[int(r.choice(len(pieces), p=w))]
+            buf += pieces[draw()]
         return bytes(buf[:L])
 
     toks = _fill_unique(rng, singles, n_extra, one)

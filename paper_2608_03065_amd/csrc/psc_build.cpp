@@ -33,7 +33,11 @@
 // states whose class can no longer change are marked determined (walks stop
 // there), and everything is flattened for the device.
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <exception>
+#include <memory>
+#include <thread>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -318,6 +322,7 @@ struct Builder {
     std::vector<int32_t> start_state;   // per lexer state
     std::vector<std::vector<int32_t>> goto_sources;  // per nonterminal
     int64_t states_built = 0;
+    std::atomic<int64_t> *total_states = nullptr;
 
     // per-q scratch
     std::vector<int32_t> tn_label, tn_child_beg, tn_child_end, tn_children, tn_grp_beg, tn_grp_end, tn_grps;
@@ -504,7 +509,8 @@ struct Builder {
         st_ebeg.push_back(0);
         st_eend.push_back(0);
         states_built++;
-        if (states_built > 40'000'000) throw BuildError(PSC_E_LIMIT, "automaton exceeds 40M states");
+        if (total_states && total_states->fetch_add(1) + 1 > 40'000'000)
+            throw BuildError(PSC_E_LIMIT, "automaton exceeds 40M states");
         return id;
     }
 
@@ -617,16 +623,60 @@ struct Builder {
             st_eend[gid] = (int32_t)e_sym.size();
         }
         if (verbose)
-            std::fprintf(stderr, "psc_build: q=%d groups=%zu trie=%zu states=%zu (total %lld) classes=%zu\n", q,
-                         groups.size(), tn_label.size(), queue.size(), (long long)states_built, masks.size());
+            std::fprintf(stderr, "psc_build: q=%d groups=%zu trie=%zu states=%zu classes=%zu\n", q,
+                         groups.size(), tn_label.size(), queue.size(), masks.size());
     }
 };
+
+// The union of the per-thread automata (Sec. 3.5: the union over all q is
+// what gets minimised).  Mask classes are re-interned globally and state ids
+// offset per builder; identical "no thread left" states of different builders
+// are merged later by minimisation.
+struct Automaton {
+    std::vector<int32_t> st_cls, st_def, st_ebeg, st_eend, e_sym, e_tgt, start_state;
+    Interner<uint32_t> masks;
+    int64_t states_built = 0;
+};
+
+Automaton merge(std::vector<std::unique_ptr<Builder>> &bs, int32_t nQ, int32_t W) {
+    Automaton A;
+    A.start_state.assign(nQ, -1);
+    std::vector<uint32_t> zero(W, 0);
+    bool added;
+    A.masks.find_or_add(zero.data(), W, &added);
+    for (auto &bp : bs) {
+        Builder &B = *bp;
+        std::vector<int32_t> cmap(B.masks.size());
+        for (size_t c = 0; c < B.masks.size(); c++)
+            cmap[c] = A.masks.find_or_add(B.masks.data((int32_t)c), W, &added);
+        B.masks.clear();
+        int32_t off = (int32_t)A.st_cls.size();
+        int32_t eoff = (int32_t)A.e_sym.size();
+        for (size_t s = 0; s < B.st_cls.size(); s++) {
+            A.st_cls.push_back(cmap[B.st_cls[s]]);
+            A.st_def.push_back(off + B.st_def[s]);
+            A.st_ebeg.push_back(eoff + B.st_ebeg[s]);
+            A.st_eend.push_back(eoff + B.st_eend[s]);
+        }
+        for (size_t e = 0; e < B.e_sym.size(); e++) {
+            A.e_sym.push_back(B.e_sym[e]);
+            A.e_tgt.push_back(off + B.e_tgt[e]);
+        }
+        for (int32_t q = 0; q < nQ; q++)
+            if (B.start_state[q] >= 0) A.start_state[q] = off + B.start_state[q];
+        A.states_built += B.states_built;
+        B.st_cls.clear(); B.st_def.clear(); B.st_ebeg.clear(); B.st_eend.clear();
+        B.e_sym.clear(); B.e_tgt.clear();
+        B.st_cls.shrink_to_fit(); B.e_sym.shrink_to_fit(); B.e_tgt.shrink_to_fit();
+    }
+    return A;
+}
 
 // ---------------------------------------------------------- minimisation
 
 // Moore refinement over total transition functions (default + explicit
 // edges); block 0..n-1 ids returned per state.
-std::vector<int32_t> minimise(const Builder &B, int32_t *n_blocks_out) {
+std::vector<int32_t> minimise(const Automaton &B, int32_t *n_blocks_out) {
     int32_t N = (int32_t)B.st_cls.size();
     std::vector<int32_t> block(N);
     {
@@ -689,9 +739,35 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         bool verbose = std::getenv("PSC_BUILD_VERBOSE") != nullptr;
         Completions C = completions(G);
         VocabTrie VT = vocab_trie(vocab);
-        Builder B(G, vocab, C, VT, verbose);
-        B.start_state.assign(G.nQ, -1);
-        for (int32_t q = 0; q < G.nQ; q++) B.build_for_lexer_state(q);
+        int32_t n_threads = (int32_t)std::thread::hardware_concurrency();
+        if (const char *e = std::getenv("PSC_BUILD_THREADS")) n_threads = std::atoi(e);
+        n_threads = std::max(1, std::min({n_threads, 32, G.nQ}));
+        std::vector<std::unique_ptr<Builder>> builders;
+        for (int32_t t = 0; t < n_threads; t++) {
+            builders.emplace_back(new Builder(G, vocab, C, VT, verbose));
+            builders.back()->start_state.assign(G.nQ, -1);
+        }
+        std::atomic<int32_t> next_q{0};
+        std::atomic<int64_t> total_states{0};
+        std::vector<std::exception_ptr> errs(n_threads);
+        auto work = [&](int32_t t) {
+            try {
+                Builder &Bt = *builders[t];
+                Bt.total_states = &total_states;
+                for (int32_t q; (q = next_q.fetch_add(1)) < G.nQ;) Bt.build_for_lexer_state(q);
+            } catch (...) {
+                errs[t] = std::current_exception();
+                next_q.store(G.nQ);
+            }
+        };
+        std::vector<std::thread> pool;
+        for (int32_t t = 1; t < n_threads; t++) pool.emplace_back(work, t);
+        work(0);
+        for (auto &th : pool) th.join();
+        for (auto &e : errs)
+            if (e) std::rethrow_exception(e);
+        Automaton B = merge(builders, G.nQ, (vocab->n_tokens + 31) / 32);
+        builders.clear();
 
         int32_t nb = 0;
         std::vector<int32_t> block = minimise(B, &nb);
@@ -774,8 +850,26 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             }
         }
 
-        // keep only the classes a walk can end in, renumbered densely
-        // (class 0, the all-zero row, always keeps id 0)
+        // Canonical order: breadth-first from the start states of q = 0, 1, ...
+        // (default successor first, then edges by symbol).  Block and class
+        // ids above depend on thread scheduling; everything emitted below is
+        // numbered in this order, so the output is identical on every build.
+        // Blocks no start state reaches are never walked and are dropped.
+        std::vector<int32_t> order;
+        {
+            std::vector<uint8_t> seen(nb, 0);
+            auto push = [&](int32_t b) { if (!seen[b]) { seen[b] = 1; order.push_back(b); } };
+            for (int32_t q = 0; q < G.nQ; q++) push(block[B.start_state[q]]);
+            for (size_t k = 0; k < order.size(); k++) {
+                int32_t b = order[k];
+                if (det[b] >= 0) continue;
+                push(m_def[b]);
+                for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) push(m_tgt[e]);
+            }
+        }
+
+        // keep only the classes a walk can end in, renumbered densely in the
+        // canonical order (class 0, the all-zero row, always keeps id 0)
         std::vector<int32_t> cls_map(B.masks.size(), -1);
         std::vector<int32_t> kept{0};
         cls_map[0] = 0;
@@ -783,7 +877,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             if (cls_map[c] < 0) { cls_map[c] = (int32_t)kept.size(); kept.push_back(c); }
             return cls_map[c];
         };
-        for (int32_t b = 0; b < nb; b++) {
+        for (int32_t b : order) {
             m_cls[b] = keep(m_cls[b]);
             if (det[b] >= 0) det[b] = keep(det[b]);
         }
@@ -799,7 +893,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         std::vector<int32_t> ref(nb, 0);
         int64_t off = G.nQ + (G.nQ & 1);
         int32_t rows = 0, dense = 0, max_sparse = 0;
-        for (int32_t b = 0; b < nb; b++) {
+        for (int32_t b : order) {
             if (det[b] >= 0) { ref[b] = class_ref(det[b]); continue; }
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             bool is_dense = ne > kSparseMax;
@@ -812,7 +906,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         }
         h->table.assign((size_t)off + kTablePad, 0);
         for (int32_t q = 0; q < G.nQ; q++) h->table[q] = ref[block[B.start_state[q]]];
-        for (int32_t b = 0; b < nb; b++) {
+        for (int32_t b : order) {
             if (det[b] >= 0) continue;
             int32_t *row = h->table.data() + ref_offset(ref[b]);
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
@@ -832,6 +926,27 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
                 }
             }
         }
+        // Skip chains: a sparse row with no edges sends every symbol to its
+        // default, and default transitions accept nothing new, so the class
+        // is constant along a chain of such rows.  Its header then holds the
+        // chain length L (row[3]) and the state reached after L symbols
+        // (row[2]); a walk consumes the L symbols with one load.
+        int32_t max_chain = 0;
+        for (int32_t b : order) {
+            if (det[b] >= 0 || ref_is_dense(ref[b]) || m_ebeg[b + 1] != m_ebeg[b]) continue;
+            int32_t L = 0, cur = b;
+            while (true) {
+                bool skip = det[cur] < 0 && !ref_is_dense(ref[cur]) && m_ebeg[cur + 1] == m_ebeg[cur];
+                if (!skip || (L > 0 && m_cls[cur] != m_cls[b]) || L >= (1 << 20)) break;
+                L++;
+                cur = m_def[cur];
+                if (cur == b) throw BuildError(PSC_E_LIMIT, "cycle of edge-free rows");
+            }
+            int32_t *row = h->table.data() + ref_offset(ref[b]);
+            row[2] = ref[cur];
+            row[3] = L;
+            max_chain = std::max(max_chain, L);
+        }
         h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);
         for (int32_t c = 0; c < h->n_classes; c++)
             std::copy(B.masks.data(kept[c]), B.masks.data(kept[c]) + h->W,
@@ -845,7 +960,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         I.n_lr_states = G.nPi;
         I.n_classes = h->n_classes;
         I.dfa_states_built = B.states_built;
-        I.dfa_states = nb;
+        I.dfa_states = (int32_t)order.size();
         I.dfa_rows = rows;
         I.dense_rows = dense;
         I.max_sparse_edges = max_sparse;
@@ -895,6 +1010,16 @@ extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stac
             if (ref_is_class(ref)) { cls = ref_class(ref); break; }
             const int32_t *row = T + ref_offset(ref);
             if (i < 0) { cls = row[0]; break; }
+            if (!ref_is_dense(ref) && row[1] == 0) {      // skip chain of row[3] symbols
+                int32_t L = row[3], t = std::min(L, i + 1);
+                bool bad = false;
+                for (int32_t k = 0; k < t; k++) bad |= st[i - k] < 0 || st[i - k] >= h->n_lr;
+                if (bad) { cls = -1; break; }
+                i -= t;
+                if (t < L) { cls = row[0]; break; }
+                ref = row[2];
+                continue;
+            }
             int32_t X = st[i--];
             if (X < 0 || X >= h->n_lr) { cls = -1; break; }
             if (ref_is_dense(ref)) {

@@ -26,17 +26,41 @@ __device__ __forceinline__ int wave_sum(int v) {
     return v;
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming (non-temporal) 16-byte accesses: the logits and mask rows are
+// touched once per step, so they should not evict the classifier table.
+__device__ __forceinline__ void store_nt(uint4 *p, uint4 v) {
+    u32x4 x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4 *>(p));
+}
+__device__ __forceinline__ uint4 load_nt(const uint4 *p) {
+    u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(x.x, x.y, x.z, x.w);
+}
+
 // One workgroup per (sequence b, slice of the mask row).  Wavefront 0 walks
 // the classifier for sequence b (every slice of the same b repeats the walk,
 // which costs latency but no bandwidth), then the whole workgroup copies its
 // slice of the class's precomputed mask row into out_bitmask[b].
 //
 // Walk (Algorithm 2, classification step): ref = start[q]; read the stack
-// top-first; each step loads the current row once -- a sparse row as one
-// wavefront-wide load of up to 64 (symbol, ref) pairs matched with a ballot,
-// a dense row as one indexed load -- and stops as soon as ref names a class
-// (a determined state).  The stack is staged 64 symbols at a time in VGPRs
-// (lane j holds the j-th symbol from the current top) and read with readlane.
+// top-first; stop as soon as ref names a class (a determined state).  The
+// walk is a chain of dependent loads, so every step is exactly ONE
+// wavefront-wide vector load of the current row:
+//   sparse row: lane 0 <- (end_class, n_edges), lane 1 <- (default, skip),
+//               lane j >= 2 <- edge j-2 as (symbol, ref); the edge matching
+//               the symbol is found with a ballot and read with readlane;
+//   dense row:  lane 0 <- (end_class, -), lane 1 <- entry[symbol];
+//   edge-free sparse row: a skip chain, L symbols consumed at once (only
+//               range checked).
+// Before the walk: round trip 1 fetches lens[b], qs[b] and the lengths before
+// b (start offset); round trip 2 fetches the top kChunk stack symbols (lane j
+// holds the j-th symbol below the chunk's top) together with start[q] in
+// lane 63.
+constexpr int kChunk = kWave - 1;
+static_assert(kSparseMax <= kWave - 2, "a sparse row must fit one wavefront load");
+
 __global__ void __launch_bounds__(kBlock)
 walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks,
                    int32_t mask_stride, int32_t n_lex, int32_t n_lr,
@@ -48,37 +72,73 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
     const int tid = threadIdx.x;
     if (tid < kWave) {
         const int lane = tid;
-        // start offset of stack b: sum of the lengths before it
-        int part = 0;
-        for (int i = lane; i < b; i += kWave) part += lens[i];
+        // round trip 1 (all independent; vector loads so no scalar load
+        // queues behind the reduction)
+        const int own = *((lane & 1) ? qs + b : lens + b);
+        int part = lane < b ? lens[lane] : 0;
+        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+        const int len = __builtin_amdgcn_readlane(own, 0);
+        const int q = __builtin_amdgcn_readlane(own, 1);
         const int off = wave_sum(part);
-        const int len = lens[b];
-        const int q = qs[b];
         int cls = -1;   // -1 = fault
         if (len > 0 && q >= 0 && q < n_lex) {
             const int32_t *st = stacks + off;
-            int ref = table[q];
             int i = len - 1;           // index of the next symbol to read
             int chunk_base = i;        // stack index held by lane 0
-            int sym = (chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
+            // round trip 2: stack chunk + start[q]
+            const int32_t *a0 = lane == kChunk ? table + q
+                              : (chunk_base - lane >= 0 ? st + (chunk_base - lane) : table + q);
+            int sym = *a0;
+            int ref = __builtin_amdgcn_readlane(sym, kChunk);
             for (;;) {
                 if (ref < 0) { cls = -ref - 1; break; }
-                const int32_t *row = table + (ref & ~1);
-                if (i < 0) { cls = row[0]; break; }
-                if (chunk_base - i >= kWave) {
+                if (i >= 0 && chunk_base - i >= kChunk) {
                     chunk_base = i;
-                    sym = (chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
+                    sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
                 }
-                const int X = __builtin_amdgcn_readlane(sym, chunk_base - i);
-                if (X < 0 || X >= n_lr) break;
-                if (ref & 1) {
-                    ref = row[kRowHeader + X];
-                } else {
-                    const int n = row[1];
-                    const int2 pr = reinterpret_cast<const int2 *>(row + kRowHeader)[lane];
-                    const unsigned long long hit = __ballot(lane < n && pr.x == X);
-                    ref = hit ? __builtin_amdgcn_readlane(pr.y, __ffsll((long long)hit) - 1) : row[2];
+                const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+                const bool x_ok = X >= 0 && X < n_lr;
+                const int32_t *row = table + (ref & ~1);
+                const bool dense = ref & 1;
+                // the one load of this step: one aligned 8-byte load per lane
+                // (a dense row's lane 1 takes the aligned pair holding entry X)
+                const int Xc = x_ok ? X : 0;
+                const int ia = dense ? (lane == 0 ? 0 : kRowHeader + (Xc & ~1)) : 2 * lane;
+                const int2 v = *reinterpret_cast<const int2 *>(row + ia);
+                const int va = v.x, vc = v.y;
+                if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); break; }
+                if (dense) {
+                    if (!x_ok) break;
+                    ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
+                    i--;
+                    continue;
                 }
+                const int n = __builtin_amdgcn_readlane(vc, 0);
+                if (n == 0) {                                    // skip chain
+                    const int L = max(__builtin_amdgcn_readlane(vc, 1), 1);   // >= 1: always progresses
+                    const int t = min(L, i + 1);
+                    int left = t;
+                    bool bad = false;
+                    while (left > 0) {
+                        if (chunk_base - i >= kChunk) {
+                            chunk_base = i;
+                            sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
+                        }
+                        const int pos = chunk_base - i;
+                        const int take = min(left, kChunk - pos);
+                        bad |= __ballot(lane >= pos && lane < pos + take && (sym < 0 || sym >= n_lr)) != 0;
+                        i -= take;
+                        left -= take;
+                    }
+                    if (bad) break;
+                    if (t < L) { cls = __builtin_amdgcn_readlane(va, 0); break; }
+                    ref = __builtin_amdgcn_readlane(va, 1);
+                    continue;
+                }
+                if (!x_ok) break;
+                const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
+                ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
+                          : __builtin_amdgcn_readlane(va, 1);
                 i--;
             }
         }
@@ -101,7 +161,7 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
         // W % 4 == 0 and out is 16-byte aligned: 128-bit loads and stores
         const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
         uint4 *d4 = reinterpret_cast<uint4 *>(dst);
-        for (int w = w0 / 4 + tid; w < w1 / 4; w += kBlock) d4[w] = s4[w];
+        for (int w = w0 / 4 + tid; w < w1 / 4; w += kBlock) store_nt(d4 + w, load_nt(s4 + w));
     } else {
         for (int w = w0 + tid; w < w1; w += kBlock) dst[w] = src[w];
     }
@@ -114,58 +174,62 @@ constexpr uint32_t kF32NegInf = 0xFF800000u;
 
 // Fast path: V % 32 == 0 and 16-byte aligned logits, so the flat element
 // index is exactly 32 x the flat mask-word index and rows never split a
-// vector.  Each wavefront owns 64 consecutive mask words (2048 elements) and
-// writes them as contiguous 1 KiB vector stores; lanes get their 8 (bf16) or
+// vector.  Each wavefront owns 64 (bf16) or 32 (fp32) consecutive mask words
+// and writes them as kVecs contiguous 1 KiB vector stores; lanes get their 8 (bf16) or
 // 4 (fp32) mask bits from the owning lane by a cross-lane shuffle.  Entries
 // whose bit is set are never touched: an all-zero group is one store of
-// -inf, a mixed group is a read-select-write of that 16-byte vector only.
+// -inf, a mixed group is a read-select-write of that 16-byte vector only
+// (all of a lane's reads are issued before its stores).
 template <bool kBf16>
 __global__ void __launch_bounds__(kBlock)
 apply_fast_kernel(uint4 *__restrict__ logits, const uint32_t *__restrict__ bits, int64_t n_words) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t seg = (int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
-    const int64_t w_base = seg * kWave;
-    if (w_base >= n_words) return;
-    const int64_t wi = w_base + lane;
-    const uint32_t m = wi < n_words ? bits[wi] : 0xFFFFFFFFu;
     constexpr int kPerVec = kBf16 ? 8 : 4;          // elements per 16-byte vector
-    constexpr int kIters = 32 / kPerVec;            // vectors per mask word
+    constexpr int kVecsPerWord = 32 / kPerVec;
+    constexpr int kVecs = 4;                        // vectors per lane
+    constexpr int kWordsPerWave = kWave * kVecs / kVecsPerWord;
     constexpr uint32_t kFull = (1u << kPerVec) - 1;
-    uint4 *base = logits + w_base * kIters;         // 16-byte vectors
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    const int64_t w_base = wave * kWordsPerWave;
+    if (w_base >= n_words) return;
+    uint32_t m = 0xFFFFFFFFu;                       // words past the end: nothing to do
+    if (lane < kWordsPerWave && w_base + lane < n_words) m = bits[w_base + lane];
+    uint4 *base = logits + w_base * kVecsPerWord;
+    uint32_t g[kVecs];
+    uint4 x[kVecs];
 #pragma unroll
-    for (int j = 0; j < kIters; j++) {
+    for (int j = 0; j < kVecs; j++) {
         // vector v = j*64 + lane covers elements [kPerVec*v, kPerVec*v + kPerVec)
         const int v = j * kWave + lane;
-        const int src_lane = v / kIters;
-        const int shift = (v % kIters) * kPerVec;
-        const uint32_t g = (__shfl(m, src_lane, kWave) >> shift) & kFull;
-        if (g == kFull) continue;
-        if (w_base + src_lane >= n_words) continue;
-        uint4 *p = base + v;
-        if (g == 0) {
-            if (kBf16) {
-                const uint32_t ni = ((uint32_t)kBf16NegInf << 16) | kBf16NegInf;
-                *p = make_uint4(ni, ni, ni, ni);
-            } else {
-                *p = make_uint4(kF32NegInf, kF32NegInf, kF32NegInf, kF32NegInf);
-            }
+        g[j] = (__shfl(m, v / kVecsPerWord, kWave) >> ((v % kVecsPerWord) * kPerVec)) & kFull;
+    }
+#pragma unroll
+    for (int j = 0; j < kVecs; j++)
+        if (g[j] != 0 && g[j] != kFull) x[j] = load_nt(base + j * kWave + lane);
+#pragma unroll
+    for (int j = 0; j < kVecs; j++) {
+        if (g[j] == kFull) continue;
+        uint4 val;
+        if (g[j] == 0) {
+            const uint32_t ni = kBf16 ? (((uint32_t)kBf16NegInf << 16) | kBf16NegInf) : kF32NegInf;
+            val = make_uint4(ni, ni, ni, ni);
         } else {
-            uint4 x = *p;
-            uint32_t *e = reinterpret_cast<uint32_t *>(&x);
+            val = x[j];
+            uint32_t *e = reinterpret_cast<uint32_t *>(&val);
             if (kBf16) {
 #pragma unroll
                 for (int k = 0; k < 4; k++) {
-                    uint32_t lo = (g >> (2 * k)) & 1 ? (e[k] & 0xFFFFu) : kBf16NegInf;
-                    uint32_t hi = (g >> (2 * k + 1)) & 1 ? (e[k] >> 16) : kBf16NegInf;
+                    const uint32_t lo = (g[j] >> (2 * k)) & 1 ? (e[k] & 0xFFFFu) : kBf16NegInf;
+                    const uint32_t hi = (g[j] >> (2 * k + 1)) & 1 ? (e[k] >> 16) : kBf16NegInf;
                     e[k] = lo | (hi << 16);
                 }
             } else {
 #pragma unroll
                 for (int k = 0; k < 4; k++)
-                    if (!((g >> k) & 1)) e[k] = kF32NegInf;
+                    if (!((g[j] >> k) & 1)) e[k] = kF32NegInf;
             }
-            *p = x;
         }
+        store_nt(base + j * kWave + lane, val);
     }
 }
 
@@ -264,8 +328,13 @@ extern "C" psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32
     const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
     if (fast) {
         const int64_t n_words = (int64_t)B * W;
-        const int64_t segs = (n_words + kWave - 1) / kWave;
-        const int64_t blocks = (segs + (kBlock / kWave) - 1) / (kBlock / kWave);
+        const int64_t words_per_wave = bf16 ? 64 : 32;           // 4 vectors per lane
+        const int64_t waves = (n_words + words_per_wave - 1) / words_per_wave;
+        const int64_t blocks = (waves + (kBlock / kWave) - 1) / (kBlock / kWave);
+        if (blocks > 0x7FFFFFFF) {
+            set_error("psc_apply_mask: tensor too large");
+            return PSC_E_INVALID_ARG;
+        }
         if (bf16)
             hipLaunchKernelGGL(apply_fast_kernel<true>, dim3((unsigned)blocks), dim3(kBlock), 0, s,
                                reinterpret_cast<uint4 *>(logits), bitmask, n_words);

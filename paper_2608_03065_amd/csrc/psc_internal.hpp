@@ -17,12 +17,16 @@ namespace psc {
 //   ref <  0 : the state is determined -- every stack continuation ends in
 //              the same class -- and that class is (-ref - 1).
 // Row header (4 int32): end_class, n_edges (sparse) or -1 (dense),
-// default_ref (sparse), reserved.  Sparse rows follow with n_edges pairs
+// default_ref (sparse), skip.  Sparse rows follow with n_edges pairs
 // (symbol, ref); dense rows with n_lr_states refs indexed by symbol.
+// A sparse row with n_edges == 0 heads a skip chain: every symbol leads to
+// the default and the class cannot change, so skip = L >= 1 symbols are
+// consumed at once and default_ref is the state reached after them (if the
+// stack ends inside the chain, the class is this row's end_class).
 // Rows start at even offsets so a pair is one aligned 8-byte load.
 constexpr int kRowHeader = 4;
-constexpr int kSparseMax = 64;      // one wavefront-wide load per step
-constexpr int kTablePad = 2 * kSparseMax + kRowHeader;  // speculative over-read
+constexpr int kSparseMax = 62;      // header + edges in one wavefront-wide load
+constexpr int kTablePad = 2 * 64 + kRowHeader;  // a row load reads 128 int32 speculatively
 
 inline bool ref_is_class(int32_t ref) { return ref < 0; }
 inline int32_t ref_class(int32_t ref) { return -ref - 1; }

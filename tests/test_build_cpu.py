@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     assert sorted(psc.EXPORTED) == names
 
 
-@pytest.mark.parametrize("name,steps", [("arithmetic", 200), ("json", 40)])
+@pytest.mark.parametrize("name,steps", [("arithmetic", 200), ("json", 40), ("schema", 6)])
 def test_host_walk_matches_oracle(name, steps):
     wl = configs.get(name)
     clf = Classifier(wl.grammar, wl.vocab)
@@ -130,3 +130,16 @@ def test_compute_masks_requires_binding():
     st = psc.lib().psc_compute_masks(clf._h, C.addressof(dummy), C.addressof(dummy), C.addressof(dummy), 1,
                                      C.addressof(dummy), None)
     assert st == -6
+
+
+def test_build_is_deterministic():
+    # class ids and table layout must not depend on thread scheduling
+    wl = configs.get("json")
+    states = [st for s in range(20) for st in wl.states(s)]
+    outs = []
+    for _ in range(3):
+        clf = Classifier(wl.grammar, wl.vocab)
+        inf = clf.info()
+        rows = np.stack([clf.class_mask(c) for c in range(inf["n_classes"])])
+        outs.append((clf.classify_host(states).tobytes(), rows.tobytes(), inf["table_bytes"]))
+    assert outs[0] == outs[1] == outs[2]

@@ -46,14 +46,24 @@ def test_arithmetic_all_steps_bit_exact(built):
     assert clf.error_count() == 0
 
 
-def test_json_steps_bit_exact(built):
-    wl, clf, orc = built("json")
-    for step in range(0, 60, 3):
+@pytest.mark.parametrize("name,steps", [("json", range(0, 60, 3)), ("schema", range(0, 1000, 50))])
+def test_full_shape_steps_bit_exact(built, name, steps):
+    """Every row of every listed step at the workload's full batch and
+    vocabulary (the shape the benchmark times), one launch per step."""
+    wl, clf, orc = built(name)
+    for step in steps:
         states = wl.states(step)
         got = _device_masks(clf, states)
         want = orc.masks(states)
-        assert np.array_equal(got, want), step
+        bad = np.nonzero((got != want).any(axis=1))[0]
+        assert bad.size == 0, (step, bad[:8])
     assert clf.error_count() == 0
+
+
+def test_schema_many_steps_in_one_launch(built):
+    wl, clf, orc = built("schema")
+    states = [st for s in range(1000, 1010) for st in wl.states(s)]
+    assert np.array_equal(_device_masks(clf, states), orc.masks(states))
 
 
 def test_device_matches_host_walk_many_steps(built):
@@ -141,11 +151,14 @@ def test_apply_matches_closed_form(B, V, dtype):
     assert (buf[B * V:].cpu() == 7).all()
 
 
-def test_apply_after_compute_end_to_end(built):
-    wl, clf, orc = built("json")
-    states = wl.states(7)
+@pytest.mark.parametrize("name,step", [("arithmetic", 5), ("json", 7), ("schema", 3), ("schema", 777)])
+def test_apply_after_compute_end_to_end(built, name, step):
+    """The whole step (compute_masks then apply_mask on one stream) against
+    the oracle's masks applied by the closed form."""
+    wl, clf, orc = built(name)
+    states = wl.states(step)
     stacks, lens, qs = pack_states(states, DEV)
-    logits = wl.logits(7)
+    logits = wl.logits(step)
     dev = logits.to(DEV)
     bm = clf.compute_masks(stacks, lens, qs)
     apply_mask(dev, bm)
