@@ -13,7 +13,7 @@ from typing import Callable
 
 import numpy as np
 
-from . import documents, grammars, schema, vocab
+from . import documents, grammars, pylike, schema, vocab
 from .grammar import GrammarTables
 from .native import HostParser
 from .seeds import rng_for
@@ -136,6 +136,54 @@ SCHEMA = _register(Workload(
     make_grammar=_c3_grammar, make_vocab=_c3_vocab, make_document=_c3_doc, doc_pool=4096,
     description="schema-conformant JSON (seeded schema: 10 object types, 5 levels); "
                 "V=151,936; B=64; bf16 N(0,2)"))
+
+
+def _c4_vocab(g):
+    return pylike.pylike_vocab(rng_for(3, salt=0x70C), 128256)
+
+
+def _c4_doc(rng, wl):
+    return pylike.program(rng)
+
+
+PYLIKE = _register(Workload(
+    3, "pylike", B=128, steps=500, logits_dtype="bf16", logits_std=2.0,
+    make_grammar=pylike.grammar, make_vocab=_c4_vocab, make_document=_c4_doc, doc_pool=2048,
+    description="Python-like CFG (88 terminals, 14 binary precedence levels, INDENT/DEDENT); "
+                "V=128,256; B=128; bf16 N(0,2)"))
+
+
+class _DeepWorkload(Workload):
+    """Prefixes that reach a target stack depth d ~ U{1..1000}: the first
+    position of a deeply nesting program where the stack has d symbols, then
+    a cut a few bytes further (inside the next lexeme more often than not)."""
+
+    @functools.cached_property
+    def depth_profiles(self) -> list:
+        return [self.host.depths(d) for d in self.documents]
+
+    def prefix(self, step: int, b: int) -> bytes:
+        rng = rng_for(self.index, step, b)
+        i = int(rng.integers(0, self.doc_pool))
+        doc, prof = self.documents[i], self.depth_profiles[i]
+        d = int(rng.integers(1, 1001))
+        p = int(np.argmax(prof >= d)) if (prof >= d).any() else len(doc)
+        cut = min(len(doc), p + int(rng.integers(0, 5)))
+        return doc[:cut]
+
+
+def _c5_vocab(g):
+    return pylike.pylike_vocab(rng_for(4, salt=0x70C), 262144)
+
+
+def _c5_doc(rng, wl):
+    return pylike.deep_program(rng, approx_chars=4500)
+
+
+STRESS = _register(_DeepWorkload(
+    4, "stress", B=256, steps=1000, logits_dtype="bf16", logits_std=2.0,
+    make_grammar=pylike.grammar, make_vocab=_c5_vocab, make_document=_c5_doc, doc_pool=256,
+    description="Python-like CFG, deep nesting (stack depth ~ U{1..1000}); V=262,144; B=256; bf16 N(0,2)"))
 
 
 def get(name: str) -> Workload:

@@ -37,7 +37,9 @@ class GrammarError(ValueError):
 
 
 class ConflictError(GrammarError):
-    pass
+    def __init__(self, msg, conflicts=()):
+        super().__init__(msg)
+        self.conflicts = list(conflicts)
 
 
 @dataclass
@@ -176,8 +178,15 @@ class Grammar:
 
         prods = [(nt_index[aug], ((False, nt_index[self.start]),))]
         prods += [(nt_index[lhs], tuple(enc(s) for s in body)) for lhs, body in self._rules]
-        action, goto = lalr1(prods, len(term_names), len(nts), end_id, nt_index[aug])
         names = [(aug, (self.start,))] + list(self._rules)
+        try:
+            action, goto = lalr1(prods, len(term_names), len(nts), end_id, nt_index[aug])
+        except ConflictError as e:
+            det = []
+            for s, t, a, b in e.conflicts[:5]:
+                rs = [names[x >> 2] for x in (a, b) if (x & 3) == 2]
+                det.append(f"state {s} on {term_names[t]}: reductions {rs}")
+            raise ConflictError(str(e) + "; " + " | ".join(det), e.conflicts) from None
         return GrammarTables(
             lexer=lexer,
             terminal_names=term_names,
@@ -355,7 +364,12 @@ def lalr1(prods, n_terms: int, n_nts: int, end_id: int, aug_nt: int):
                 la >>= 1
                 t += 1
     if conflicts:
-        raise ConflictError(f"{len(conflicts)} LALR(1) conflicts, first: {conflicts[:5]}")
+        def show(a):
+            k = a & 3
+            return ("shift" if k == 1 else "reduce" if k == 2 else "accept") + f" {a >> 2}"
+        first = [(s, t, show(a), show(b)) for s, t, a, b in conflicts[:5]]
+        raise ConflictError(f"{len(conflicts)} LALR(1) conflicts (state, terminal, action, action): {first}",
+                            conflicts)
     return action.astype(np.int32), goto.astype(np.int32)
 
 

@@ -184,3 +184,21 @@ void hs_viable_batch(const hs_grammar *g, const uint8_t *bytes, const int64_t *o
         free(st.s);
     }
 }
+
+/* Stack length after every prefix text[0..i), i = 0..len (depths has len+1
+ * entries).  Returns HS_OK or the first error (later depths are -1). */
+int hs_depths(const hs_grammar *g, const uint8_t *text, int64_t len, int32_t *depths) {
+    stk st = {0, 0, 0};
+    int32_t cur = 0;
+    int rc = HS_OK;
+    if (!stk_push(&st, 0)) return HS_CAPACITY;
+    for (int64_t i = 0; i <= len; i++) depths[i] = -1;
+    depths[0] = 1;
+    for (int64_t i = 0; i < len; i++) {
+        rc = lex_byte(g, &cur, &st, text[i]);
+        if (rc != HS_OK) break;
+        depths[i + 1] = (int32_t)st.n;
+    }
+    free(st.s);
+    return rc;
+}

@@ -46,6 +46,8 @@ def lib():
         _lib.hs_accepts.restype = C.c_int
         _lib.hs_accepts_batch.argtypes = [P, P, P, C.c_int64, P]
         _lib.hs_viable_batch.argtypes = [P, P, P, C.c_int64, P]
+        _lib.hs_depths.argtypes = [P, P, C.c_int64, P]
+        _lib.hs_depths.restype = C.c_int
     return _lib
 
 
@@ -95,6 +97,15 @@ class HostParser:
 
     def state(self, text: bytes) -> tuple[int, np.ndarray]:
         return self.states_at(text, [len(text)])[0]
+
+    def depths(self, text: bytes) -> np.ndarray:
+        """Parser stack length after every prefix text[:i], i = 0..len."""
+        buf = np.frombuffer(text, dtype=np.uint8) if text else np.zeros(1, np.uint8)
+        out = np.zeros(len(text) + 1, np.int32)
+        rc = lib().hs_depths(self._sp, _ptr(buf), len(text), _ptr(out))
+        if rc != 0:
+            raise ValueError(f"text does not lex/parse (code {rc})")
+        return out
 
     def accepts(self, text: bytes) -> bool:
         buf = np.frombuffer(text, dtype=np.uint8) if text else np.zeros(1, np.uint8)

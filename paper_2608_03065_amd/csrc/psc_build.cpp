@@ -305,6 +305,60 @@ inline int32_t th_node(uint64_t t) { return (int32_t)(t >> 32); }
 inline int32_t th_k(uint64_t t) { return (int32_t)((t >> 16) & 0xFFFF); }
 inline int32_t th_A(uint64_t t) { return (int32_t)(t & 0xFFFF); }
 
+// Moore refinement over total transition functions (default + explicit
+// edges).  States start in blocks of equal `label`; returns the block of
+// every state (ids 0..*n_blocks-1).
+std::vector<int32_t> moore(int32_t N, const std::vector<int32_t> &label, const std::vector<int32_t> &def,
+                           const std::vector<int32_t> &ebeg, const std::vector<int32_t> &eend,
+                           const std::vector<int32_t> &esym, const std::vector<int32_t> &etgt,
+                           int32_t *n_blocks_out) {
+    std::vector<int32_t> block(N);
+    int32_t nb;
+    {
+        Interner<int32_t> in;
+        bool a;
+        for (int32_t s = 0; s < N; s++) block[s] = in.find_or_add(&label[s], 1, &a);
+        nb = (int32_t)in.size();
+    }
+    std::vector<int32_t> sig, nbk(N);
+    while (true) {
+        Interner<int32_t> in;
+        for (int32_t s = 0; s < N; s++) {
+            sig.clear();
+            int32_t db = block[def[s]];
+            sig.push_back(block[s]);
+            sig.push_back(db);
+            for (int32_t e = ebeg[s]; e < eend[s]; e++) {
+                int32_t tb = block[etgt[e]];
+                if (tb != db) { sig.push_back(esym[e]); sig.push_back(tb); }
+            }
+            bool a;
+            nbk[s] = in.find_or_add(sig.data(), sig.size(), &a);
+        }
+        int32_t nnb = (int32_t)in.size();
+        block.swap(nbk);
+        if (nnb == nb) break;
+        nb = nnb;
+    }
+    *n_blocks_out = nb;
+    return block;
+}
+
+// The stack known to a running simulation (top at the back); bounded by the
+// longest realizable terminal sequence plus the pushes of its reductions.
+constexpr int32_t kMaxBeta = 192;
+struct Beta {
+    int32_t n = 0;
+    int32_t s[kMaxBeta];
+    void push(int32_t v) {
+        if (n >= kMaxBeta) throw BuildError(PSC_E_LIMIT, "simulated stack exceeds 192 symbols");
+        s[n++] = v;
+    }
+    int32_t top() const { return s[n - 1]; }
+};
+
+// One builder per thread; it processes lexer states one at a time and
+// appends each one's minimised sub-automaton to its output arrays.
 struct Builder {
     const Gram &G;
     const psc_vocab *vocab;
@@ -313,26 +367,49 @@ struct Builder {
     int32_t V, W;
     bool verbose;
 
-    // global mask classes (class 0 = all zero)
+    // outputs: mask classes (class 0 = all zero) and automaton states
     Interner<uint32_t> masks;
-    // global automaton states
     std::vector<int32_t> st_cls, st_def, st_ebeg, st_eend;
     std::vector<int32_t> e_sym, e_tgt;
-    std::unordered_map<int32_t, int32_t> empty_state_of_cls;
     std::vector<int32_t> start_state;   // per lexer state
     std::vector<std::vector<int32_t>> goto_sources;  // per nonterminal
     int64_t states_built = 0;
     std::atomic<int64_t> *total_states = nullptr;
 
-    // per-q scratch
+    // per-q: trie of realizable terminal sequences
     std::vector<int32_t> tn_label, tn_child_beg, tn_child_end, tn_children, tn_grp_beg, tn_grp_end, tn_grps;
     std::vector<std::vector<int32_t>> grp_tokens;
-    Interner<uint64_t> qstates;          // key: [cls, threads...]
-    std::vector<int32_t> qstate_global;  // qstate id -> global state id
-    std::unordered_map<uint64_t, int32_t> add_memo;  // (cls, node) -> cls
+    std::vector<uint64_t> node_ka, node_kb;        // random keys of trie nodes
+
+    // per-q: subset states.  A state is (waiting threads, accepted trie
+    // nodes); the accepted set is identified by a 128-bit order-independent
+    // hash (XOR of node keys -- a node is accepted at most once along a
+    // walk) and reconstructed, when needed, from the breadth-first tree:
+    // each state keeps its parent and the nodes accepted on that edge.
+    Interner<uint64_t> qstates;                     // key: [acc_a, acc_b, threads...]
+    std::vector<int32_t> qs_parent, qs_dbeg, qs_dend, delta_pool;
+    std::vector<uint64_t> qs_acca, qs_accb;
+    std::vector<int32_t> qs_def, qs_ebeg, qs_eend, qe_sym, qe_tgt;
+
+    // per-q: resumption memo (trie node, symbol, nonterminal) -> results
+    std::unordered_map<uint64_t, int32_t> memo;
+    std::vector<int32_t> memo_wb, memo_we, memo_ab, memo_ae, memo_a;
+    std::vector<uint64_t> memo_w;
+
     std::vector<uint64_t> newW;
     std::vector<int32_t> acc;
-    std::vector<uint32_t> rowbuf;
+
+    // Valid stacks only: the symbol below X on a parser stack is an LR
+    // predecessor of X (it has a shift or goto into X), and the top is a
+    // shift target or the start state.  Each subset state carries the set of
+    // symbols that can come next on a valid stack (an interned bitset over
+    // Pi) and only those transitions are expanded; any other symbol belongs
+    // to no valid stack and falls to the default.
+    int32_t pw;                                       // uint64 words per symbol set
+    std::vector<uint64_t> pred_bits;                  // [nPi][pw]
+    std::vector<uint64_t> tops_bits;                  // [pw]
+    Interner<uint64_t> symsets;
+    std::vector<uint64_t> setbuf;
 
     Builder(const Gram &g, const psc_vocab *v, const Completions &c, const VocabTrie &vt, bool verb)
         : G(g), vocab(v), C(c), VT(vt), V(v->n_tokens), W((v->n_tokens + 31) / 32), verbose(verb) {
@@ -343,8 +420,32 @@ struct Builder {
         for (int32_t s = 0; s < G.nPi; s++)
             for (int32_t A = 0; A < G.nN; A++)
                 if (G.gto(s, A) >= 0) goto_sources[A].push_back(s);
-        rowbuf.resize(W);
+        pw = (G.nPi + 63) / 64;
+        pred_bits.assign((size_t)G.nPi * pw, 0);
+        tops_bits.assign(pw, 0);
+        tops_bits[0] |= 1;
+        for (int32_t s = 0; s < G.nPi; s++) {
+            for (int32_t t = 0; t < G.nT; t++) {
+                int32_t a = G.act(s, t);
+                if ((a & 3) == 1) {
+                    int32_t x = a >> 2;
+                    pred_bits[(size_t)x * pw + s / 64] |= 1ull << (s % 64);
+                    tops_bits[x / 64] |= 1ull << (x % 64);
+                }
+            }
+            for (int32_t A = 0; A < G.nN; A++) {
+                int32_t x = G.gto(s, A);
+                if (x >= 0) pred_bits[(size_t)x * pw + s / 64] |= 1ull << (s % 64);
+            }
+        }
+        setbuf.resize(pw);
     }
+
+    int32_t symset_id(const uint64_t *bits) {
+        bool a;
+        return symsets.find_or_add(bits, pw, &a);
+    }
+    bool in_set(int32_t set, int32_t X) const { return (symsets.data(set)[X / 64] >> (X % 64)) & 1; }
 
     // ---- lexical pass for one q: group tokens by (emitted x, end state p)
     void lexical_pass(int32_t q, Interner<int32_t> &groups) {
@@ -391,16 +492,15 @@ struct Builder {
     // ---- the trie of realizable terminal sequences R_q(V) for one q
     void sequence_trie(int32_t q, const Interner<int32_t> &groups) {
         std::vector<int32_t> label{-1};
-        std::vector<std::unordered_map<int32_t, int32_t>> kids(1);
-        std::vector<std::vector<int32_t>> ngrps(1);
+        std::unordered_map<uint64_t, int32_t> kid;
+        std::vector<std::pair<int32_t, int32_t>> node_grp;   // (node, group)
         auto child = [&](int32_t n, int32_t t) {
-            auto it = kids[n].find(t);
-            if (it != kids[n].end()) return it->second;
+            uint64_t k = ((uint64_t)(uint32_t)n << 32) | (uint32_t)t;
+            auto it = kid.find(k);
+            if (it != kid.end()) return it->second;
             int32_t id = (int32_t)label.size();
             label.push_back(t);
-            kids.emplace_back();
-            ngrps.emplace_back();
-            kids[n].emplace(t, id);
+            kid.emplace(k, id);
             return id;
         };
         int32_t n_groups = (int32_t)groups.size();
@@ -410,8 +510,8 @@ struct Builder {
             int32_t p = k[0];
             int32_t n = 0;
             for (size_t j = 1; j < len; j++) n = child(n, k[j]);
-            if (C.eps[p]) ngrps[n].push_back(g);
-            for (int32_t t : C.terms[p]) ngrps[child(n, t)].push_back(g);
+            if (C.eps[p]) node_grp.emplace_back(n, g);
+            for (int32_t t : C.terms[p]) node_grp.emplace_back(child(n, t), g);
         }
         // EOS: the pending lexeme must end here, then $end must be accepted
         if (vocab->eos_id >= 0) {
@@ -423,37 +523,52 @@ struct Builder {
             }
             if (n >= 0) {
                 grp_tokens.push_back({vocab->eos_id});
-                ngrps[n].push_back((int32_t)grp_tokens.size() - 1);
+                node_grp.emplace_back(n, (int32_t)grp_tokens.size() - 1);
             }
         }
         int32_t N = (int32_t)label.size();
         tn_label = label;
+        // children sorted by terminal, CSR
+        std::vector<std::pair<uint64_t, int32_t>> edges(kid.begin(), kid.end());
+        std::sort(edges.begin(), edges.end(), [&](const auto &a, const auto &b) {
+            uint32_t pa = (uint32_t)(a.first >> 32), pb = (uint32_t)(b.first >> 32);
+            return pa != pb ? pa < pb : (uint32_t)a.first < (uint32_t)b.first;
+        });
         tn_child_beg.assign(N, 0);
         tn_child_end.assign(N, 0);
         tn_children.clear();
+        for (auto &e : edges) {
+            int32_t par = (int32_t)(e.first >> 32);
+            if (tn_child_end[par] == tn_child_beg[par]) tn_child_beg[par] = (int32_t)tn_children.size();
+            tn_children.push_back(e.second);
+            tn_child_end[par] = (int32_t)tn_children.size();
+        }
+        std::sort(node_grp.begin(), node_grp.end());
         tn_grp_beg.assign(N, 0);
         tn_grp_end.assign(N, 0);
         tn_grps.clear();
+        for (auto &ng : node_grp) {
+            if (tn_grp_end[ng.first] == tn_grp_beg[ng.first]) tn_grp_beg[ng.first] = (int32_t)tn_grps.size();
+            tn_grps.push_back(ng.second);
+            tn_grp_end[ng.first] = (int32_t)tn_grps.size();
+        }
+        node_ka.resize(N);
+        node_kb.resize(N);
         for (int32_t n = 0; n < N; n++) {
-            tn_child_beg[n] = (int32_t)tn_children.size();
-            std::vector<std::pair<int32_t, int32_t>> kv(kids[n].begin(), kids[n].end());
-            std::sort(kv.begin(), kv.end());
-            for (auto &x : kv) tn_children.push_back(x.second);
-            tn_child_end[n] = (int32_t)tn_children.size();
-            tn_grp_beg[n] = (int32_t)tn_grps.size();
-            tn_grps.insert(tn_grps.end(), ngrps[n].begin(), ngrps[n].end());
-            tn_grp_end[n] = (int32_t)tn_grps.size();
+            uint64_t base = ((uint64_t)(uint32_t)q << 32) | (uint32_t)n;
+            node_ka[n] = mix64(base ^ 0x5A17C0DEull);
+            node_kb[n] = mix64(base * 0x9E3779B97F4A7C15ull + 0x1234ull);
         }
     }
 
-    // ---- parser simulation on a known stack top (beta, top at back)
-    void run(int32_t c, std::vector<int32_t> &beta) {
+    // ---- parser simulation on a known stack top (beta, top at the back)
+    void run(int32_t c, Beta &beta) {
         const int32_t t = tn_label[c];
         for (;;) {
-            int32_t a = G.act(beta.back(), t);
+            int32_t a = G.act(beta.top(), t);
             switch (a & 3) {
             case 1:                       // shift: the stack is stable again
-                beta.push_back(a >> 2);
+                beta.push(a >> 2);
                 visit(c, beta);
                 return;
             case 3:                       // accept ($end)
@@ -461,14 +576,14 @@ struct Builder {
                 return;
             case 2: {                     // reduce
                 int32_t p = a >> 2, m = G.plen[p], A = G.plhs[p];
-                if (m < (int32_t)beta.size()) {
-                    beta.resize(beta.size() - m);
-                    int32_t g = G.gto(beta.back(), A);
+                if (m < beta.n) {
+                    beta.n -= m;
+                    int32_t g = G.gto(beta.top(), A);
                     if (g < 0) return;
-                    beta.push_back(g);
+                    beta.push(g);
                     continue;
                 }
-                int32_t k = m - (int32_t)beta.size();
+                int32_t k = m - beta.n;
                 if (k > 0xFFFE) throw BuildError(PSC_E_LIMIT, "production too long");
                 newW.push_back(pack_thread(c, k, A));
                 return;
@@ -479,159 +594,264 @@ struct Builder {
         }
     }
 
-    void visit(int32_t c, const std::vector<int32_t> &beta) {
+    void visit(int32_t c, const Beta &beta) {
         if (tn_grp_end[c] > tn_grp_beg[c]) acc.push_back(c);
         for (int32_t j = tn_child_beg[c]; j < tn_child_end[c]; j++) {
-            std::vector<int32_t> b2 = beta;
+            Beta b2;
+            b2.n = beta.n;
+            std::memcpy(b2.s, beta.s, sizeof(int32_t) * beta.n);
             run(tn_children[j], b2);
         }
     }
 
-    // mask class after accepting every token of trie node c
-    int32_t add_node(int32_t cls, int32_t c) {
-        uint64_t key = ((uint64_t)(uint32_t)cls << 32) | (uint32_t)c;
-        auto it = add_memo.find(key);
-        if (it != add_memo.end()) return it->second;
-        const uint32_t *src = masks.data(cls);
-        std::copy(src, src + W, rowbuf.begin());
-        for (int32_t j = tn_grp_beg[c]; j < tn_grp_end[c]; j++)
-            for (int32_t tok : grp_tokens[tn_grps[j]]) rowbuf[tok >> 5] |= 1u << (tok & 31);
-        bool added;
-        int32_t out = masks.find_or_add(rowbuf.data(), W, &added);
-        add_memo.emplace(key, out);
-        return out;
+    // resume a thread waiting for its goto base X (memoised)
+    void resume(int32_t c, int32_t X, int32_t A) {
+        const uint64_t key = (uint64_t)(uint32_t)c * ((uint64_t)G.nPi * 32768ull) + (uint64_t)X * 32768ull + (uint64_t)A;
+        auto it = memo.find(key);
+        if (it == memo.end()) {
+            size_t w0 = newW.size(), a0 = acc.size();
+            int32_t g = G.gto(X, A);
+            if (g >= 0) {
+                Beta beta;
+                beta.n = 0;
+                beta.push(X);
+                beta.push(g);
+                run(c, beta);
+            }
+            int32_t id = (int32_t)memo_wb.size();
+            memo_wb.push_back((int32_t)memo_w.size());
+            memo_w.insert(memo_w.end(), newW.begin() + w0, newW.end());
+            memo_we.push_back((int32_t)memo_w.size());
+            memo_ab.push_back((int32_t)memo_a.size());
+            memo_a.insert(memo_a.end(), acc.begin() + a0, acc.end());
+            memo_ae.push_back((int32_t)memo_a.size());
+            memo.emplace(key, id);
+            return;
+        }
+        int32_t id = it->second;
+        newW.insert(newW.end(), memo_w.begin() + memo_wb[id], memo_w.begin() + memo_we[id]);
+        acc.insert(acc.end(), memo_a.begin() + memo_ab[id], memo_a.begin() + memo_ae[id]);
     }
 
-    int32_t new_global_state(int32_t cls) {
-        int32_t id = (int32_t)st_cls.size();
-        st_cls.push_back(cls);
-        st_def.push_back(id);
-        st_ebeg.push_back(0);
-        st_eend.push_back(0);
-        states_built++;
-        if (total_states && total_states->fetch_add(1) + 1 > 40'000'000)
-            throw BuildError(PSC_E_LIMIT, "automaton exceeds 40M states");
+    // state id for (threads, accepted set); queue new ones
+    int32_t intern(std::vector<uint64_t> &th, uint64_t acca, uint64_t accb, int32_t next_set, int32_t parent,
+                   const std::vector<int32_t> &delta, std::vector<int32_t> &queue) {
+        std::sort(th.begin(), th.end());
+        th.erase(std::unique(th.begin(), th.end()), th.end());
+        std::vector<uint64_t> key;
+        key.reserve(th.size() + 3);
+        key.push_back(acca);
+        key.push_back(accb);
+        key.push_back((uint64_t)(uint32_t)next_set);
+        key.insert(key.end(), th.begin(), th.end());
+        bool added;
+        int32_t id = qstates.find_or_add(key.data(), key.size(), &added);
+        if (added) {
+            qs_parent.push_back(parent);
+            qs_dbeg.push_back((int32_t)delta_pool.size());
+            delta_pool.insert(delta_pool.end(), delta.begin(), delta.end());
+            qs_dend.push_back((int32_t)delta_pool.size());
+            qs_acca.push_back(acca);
+            qs_accb.push_back(accb);
+            qs_def.push_back(id);
+            qs_ebeg.push_back(0);
+            qs_eend.push_back(0);
+            queue.push_back(id);
+            states_built++;
+            if (total_states && total_states->fetch_add(1) + 1 > 60'000'000)
+                throw BuildError(PSC_E_LIMIT, "automaton exceeds 60M states");
+        }
         return id;
     }
 
-    // state id for (threads, cls); queue new per-q states
-    int32_t intern(std::vector<uint64_t> &th, int32_t cls, std::vector<int32_t> &queue) {
-        std::sort(th.begin(), th.end());
-        th.erase(std::unique(th.begin(), th.end()), th.end());
-        if (th.empty()) {
-            auto it = empty_state_of_cls.find(cls);
-            if (it != empty_state_of_cls.end()) return it->second;
-            int32_t id = new_global_state(cls);   // absorbing: default is itself
-            empty_state_of_cls.emplace(cls, id);
-            return id;
-        }
-        std::vector<uint64_t> key;
-        key.reserve(th.size() + 1);
-        key.push_back((uint64_t)(uint32_t)cls);
-        key.insert(key.end(), th.begin(), th.end());
-        bool added;
-        int32_t qid = qstates.find_or_add(key.data(), key.size(), &added);
-        if (added) {
-            qstate_global.push_back(new_global_state(cls));
-            queue.push_back(qid);
-        }
-        return qstate_global[qid];
-    }
-
-    int32_t step(const uint64_t *th, size_t n, int32_t cls, int32_t X, std::vector<int32_t> &queue) {
+    int32_t step(int32_t sid, const uint64_t *th, size_t n, uint64_t acca, uint64_t accb, int32_t X,
+                 std::vector<int32_t> &queue) {
         newW.clear();
         acc.clear();
-        std::vector<int32_t> beta;
         for (size_t i = 0; i < n; i++) {
             uint64_t t = th[i];
             int32_t c = th_node(t), k = th_k(t), A = th_A(t);
             if (A == kInitA) {
                 for (int32_t j = tn_child_beg[c]; j < tn_child_end[c]; j++) {
-                    beta.assign(1, X);
+                    Beta beta;
+                    beta.n = 0;
+                    beta.push(X);
                     run(tn_children[j], beta);
                 }
             } else if (k > 0) {
                 newW.push_back(pack_thread(c, k - 1, A));
             } else {
-                int32_t g = G.gto(X, A);
-                if (g < 0) continue;
-                beta.assign({X, g});
-                run(c, beta);
+                resume(c, X, A);
             }
         }
         std::sort(acc.begin(), acc.end());
         acc.erase(std::unique(acc.begin(), acc.end()), acc.end());
-        int32_t cls2 = cls;
-        for (int32_t c : acc) cls2 = add_node(cls2, c);
+        for (int32_t c : acc) {
+            acca ^= node_ka[c];
+            accb ^= node_kb[c];
+        }
         std::vector<uint64_t> w2 = newW;
-        return intern(w2, cls2, queue);
+        return intern(w2, acca, accb, symset_id(&pred_bits[(size_t)X * pw]), sid, acc, queue);
+    }
+
+    // mask of the tokens accepted on the breadth-first path to state s
+    int32_t class_of(int32_t s, std::vector<uint32_t> &row) {
+        std::fill(row.begin(), row.end(), 0u);
+        for (int32_t x = s; x >= 0; x = qs_parent[x])
+            for (int32_t d = qs_dbeg[x]; d < qs_dend[x]; d++) {
+                int32_t c = delta_pool[d];
+                for (int32_t j = tn_grp_beg[c]; j < tn_grp_end[c]; j++)
+                    for (int32_t tok : grp_tokens[tn_grps[j]]) row[tok >> 5] |= 1u << (tok & 31);
+            }
+        bool added;
+        return masks.find_or_add(row.data(), W, &added);
+    }
+
+    void clear_q() {
+        qstates.clear();
+        qs_parent.clear(); qs_dbeg.clear(); qs_dend.clear(); delta_pool.clear();
+        qs_acca.clear(); qs_accb.clear(); qs_def.clear(); qs_ebeg.clear(); qs_eend.clear();
+        qe_sym.clear(); qe_tgt.clear();
+        memo.clear(); memo_wb.clear(); memo_we.clear(); memo_ab.clear(); memo_ae.clear();
+        memo_a.clear(); memo_w.clear();
+        for (auto *v : {&qs_parent, &qs_dbeg, &qs_dend, &delta_pool, &qs_def, &qs_ebeg, &qs_eend, &qe_sym, &qe_tgt,
+                        &memo_wb, &memo_we, &memo_ab, &memo_ae, &memo_a})
+            v->shrink_to_fit();
+        qs_acca.shrink_to_fit(); qs_accb.shrink_to_fit(); memo_w.shrink_to_fit();
+        std::unordered_map<uint64_t, int32_t>().swap(memo);
     }
 
     void build_for_lexer_state(int32_t q) {
+        auto t_start = std::chrono::steady_clock::now();
         Interner<int32_t> groups;
         lexical_pass(q, groups);
         sequence_trie(q, groups);
-        qstates.clear();
-        qstate_global.clear();
-        add_memo.clear();
+        clear_q();
         std::vector<int32_t> queue;
-        int32_t cls0 = 0;
-        if (tn_grp_end[0] > tn_grp_beg[0]) cls0 = add_node(0, 0);
+        // the root's groups (sequence x = nothing more) are accepted at once
+        std::vector<int32_t> root_acc;
+        uint64_t a0 = 0, b0 = 0;
+        if (tn_grp_end[0] > tn_grp_beg[0]) {
+            root_acc.push_back(0);
+            a0 ^= node_ka[0];
+            b0 ^= node_kb[0];
+        }
         std::vector<uint64_t> init{pack_thread(0, 0, kInitA)};
-        start_state[q] = intern(init, cls0, queue);
+        int32_t start = intern(init, a0, b0, symset_id(tops_bits.data()), -1, root_acc, queue);
         std::vector<uint64_t> key, dW;
-        std::vector<int32_t> syms;
+        std::vector<int32_t> syms, none;
         std::vector<uint8_t> seen(G.nPi, 0);
+        auto t_last = t_start;
+        size_t max_threads = 0;
         for (size_t qi = 0; qi < queue.size(); qi++) {
-            int32_t qid = queue[qi];
-            key.assign(qstates.data(qid), qstates.data(qid) + qstates.len(qid));
-            int32_t gid = qstate_global[qid];
-            int32_t cls = (int32_t)key[0];
-            const uint64_t *th = key.data() + 1;
-            size_t n = key.size() - 1;
+            if (verbose) {
+                auto now = std::chrono::steady_clock::now();
+                if (std::chrono::duration<double>(now - t_last).count() > 5.0) {
+                    t_last = now;
+                    std::fprintf(stderr, "psc_build:   q=%d %.0fs states %zu/%zu max-threads %zu memo %zu\n", q,
+                                 std::chrono::duration<double>(now - t_start).count(), qi, queue.size(),
+                                 max_threads, memo.size());
+                }
+            }
+            int32_t sid = queue[qi];
+            key.assign(qstates.data(sid), qstates.data(sid) + qstates.len(sid));
+            uint64_t acca = key[0], accb = key[1];
+            const int32_t next_set = (int32_t)key[2];
+            const uint64_t *th = key.data() + 3;
+            size_t n = key.size() - 3;
+            max_threads = std::max(max_threads, n);
             // default transition: waiting-to-skip threads advance, others die
             dW.clear();
-            bool init = false;
+            bool init_thread = false;
             syms.clear();
             for (size_t i = 0; i < n; i++) {
                 int32_t k = th_k(th[i]), A = th_A(th[i]);
-                if (A == kInitA) init = true;
+                if (A == kInitA) init_thread = true;
                 else if (k > 0) dW.push_back(pack_thread(th_node(th[i]), k - 1, A));
                 else
                     for (int32_t X : goto_sources[A])
-                        if (!seen[X]) { seen[X] = 1; syms.push_back(X); }
+                        if (!seen[X] && in_set(next_set, X)) { seen[X] = 1; syms.push_back(X); }
             }
-            if (init) {
-                for (int32_t X : syms) seen[X] = 0;
+            for (int32_t X : syms) seen[X] = 0;
+            if (init_thread) {
                 syms.clear();
-                for (int32_t X = 0; X < G.nPi; X++) syms.push_back(X);
-            } else {
-                for (int32_t X : syms) seen[X] = 0;
+                for (int32_t X = 0; X < G.nPi; X++)
+                    if (in_set(next_set, X)) syms.push_back(X);
             }
             std::sort(syms.begin(), syms.end());
-            int32_t def = intern(dW, cls, queue);
-            int32_t ebeg = (int32_t)e_sym.size();
-            for (int32_t X : syms) {
-                int32_t tgt = step(th, n, cls, X, queue);
-                if (tgt != def) {
-                    e_sym.push_back(X);
-                    e_tgt.push_back(tgt);
+            // the symbols that take the default: valid next symbols not in syms
+            std::fill(setbuf.begin(), setbuf.end(), 0ull);
+            {
+                const uint64_t *ns = symsets.data(next_set);
+                size_t j = 0;
+                for (int32_t w = 0; w < pw; w++) {
+                    uint64_t m = ns[w];
+                    while (m) {
+                        int32_t X = w * 64 + __builtin_ctzll(m);
+                        m &= m - 1;
+                        while (j < syms.size() && syms[j] < X) j++;
+                        if (j < syms.size() && syms[j] == X) continue;
+                        const uint64_t *pb = &pred_bits[(size_t)X * pw];
+                        for (int32_t k = 0; k < pw; k++) setbuf[k] |= pb[k];
+                    }
                 }
             }
-            st_def[gid] = def;
-            st_ebeg[gid] = ebeg;
-            st_eend[gid] = (int32_t)e_sym.size();
+            int32_t def = n == 0 ? sid : intern(dW, acca, accb, symset_id(setbuf.data()), sid, none, queue);
+            int32_t ebeg = (int32_t)qe_sym.size();
+            for (int32_t X : syms) {
+                int32_t tgt = step(sid, th, n, acca, accb, X, queue);
+                if (tgt != def) {
+                    qe_sym.push_back(X);
+                    qe_tgt.push_back(tgt);
+                }
+            }
+            qs_def[sid] = def;
+            qs_ebeg[sid] = ebeg;
+            qs_eend[sid] = (int32_t)qe_sym.size();
         }
+        // minimise this lexer state's automaton (accepted-set hashes as the
+        // initial partition), then compute the mask of each block once
+        int32_t N = (int32_t)queue.size();
+        std::vector<int32_t> label(N);
+        {
+            Interner<uint64_t> in;
+            bool a;
+            for (int32_t s = 0; s < N; s++) {
+                uint64_t k2[2] = {qs_acca[s], qs_accb[s]};
+                label[s] = in.find_or_add(k2, 2, &a);
+            }
+        }
+        int32_t nb = 0;
+        std::vector<int32_t> block = moore(N, label, qs_def, qs_ebeg, qs_eend, qe_sym, qe_tgt, &nb);
+        std::vector<int32_t> rep(nb, -1);
+        for (int32_t s = 0; s < N; s++)
+            if (rep[block[s]] < 0) rep[block[s]] = s;
+        std::vector<uint32_t> row(W);
+        int32_t off = (int32_t)st_cls.size();
+        for (int32_t b = 0; b < nb; b++) {
+            int32_t s = rep[b];
+            st_cls.push_back(class_of(s, row));
+            int32_t db = block[qs_def[s]];
+            st_def.push_back(off + db);
+            st_ebeg.push_back((int32_t)e_sym.size());
+            for (int32_t e = qs_ebeg[s]; e < qs_eend[s]; e++) {
+                int32_t tb = block[qe_tgt[e]];
+                if (tb != db) { e_sym.push_back(qe_sym[e]); e_tgt.push_back(off + tb); }
+            }
+            st_eend.push_back((int32_t)e_sym.size());
+        }
+        start_state[q] = off + block[start];
         if (verbose)
-            std::fprintf(stderr, "psc_build: q=%d groups=%zu trie=%zu states=%zu classes=%zu\n", q,
-                         groups.size(), tn_label.size(), queue.size(), masks.size());
+            std::fprintf(stderr, "psc_build: q=%d groups=%zu trie=%zu states=%d blocks=%d max-threads=%zu classes=%zu %.1fs\n",
+                         q, groups.size(), tn_label.size(), N, nb, max_threads, masks.size(),
+                         std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count());
+        clear_q();
     }
 };
 
 // The union of the per-thread automata (Sec. 3.5: the union over all q is
 // what gets minimised).  Mask classes are re-interned globally and state ids
-// offset per builder; identical "no thread left" states of different builders
-// are merged later by minimisation.
+// offset per builder.
 struct Automaton {
     std::vector<int32_t> st_cls, st_def, st_ebeg, st_eend, e_sym, e_tgt, start_state;
     Interner<uint32_t> masks;
@@ -674,43 +894,9 @@ Automaton merge(std::vector<std::unique_ptr<Builder>> &bs, int32_t nQ, int32_t W
 
 // ---------------------------------------------------------- minimisation
 
-// Moore refinement over total transition functions (default + explicit
-// edges); block 0..n-1 ids returned per state.
 std::vector<int32_t> minimise(const Automaton &B, int32_t *n_blocks_out) {
-    int32_t N = (int32_t)B.st_cls.size();
-    std::vector<int32_t> block(N);
-    {
-        Interner<int32_t> in;
-        for (int32_t s = 0; s < N; s++) {
-            bool a;
-            block[s] = in.find_or_add(&B.st_cls[s], 1, &a);
-        }
-    }
-    int32_t nb = 0;
-    for (int32_t b : block) nb = std::max(nb, b + 1);
-    std::vector<int32_t> sig;
-    while (true) {
-        Interner<int32_t> in;
-        std::vector<int32_t> nbk(N);
-        for (int32_t s = 0; s < N; s++) {
-            sig.clear();
-            int32_t db = block[B.st_def[s]];
-            sig.push_back(block[s]);
-            sig.push_back(db);
-            for (int32_t e = B.st_ebeg[s]; e < B.st_eend[s]; e++) {
-                int32_t tb = block[B.e_tgt[e]];
-                if (tb != db) { sig.push_back(B.e_sym[e]); sig.push_back(tb); }
-            }
-            bool a;
-            nbk[s] = in.find_or_add(sig.data(), sig.size(), &a);
-        }
-        int32_t nnb = (int32_t)in.size();
-        block.swap(nbk);
-        if (nnb == nb) break;
-        nb = nnb;
-    }
-    *n_blocks_out = nb;
-    return block;
+    return moore((int32_t)B.st_cls.size(), B.st_cls, B.st_def, B.st_ebeg, B.st_eend, B.e_sym, B.e_tgt,
+                 n_blocks_out);
 }
 
 }  // namespace
