@@ -46,7 +46,8 @@ def test_arithmetic_all_steps_bit_exact(built):
     assert clf.error_count() == 0
 
 
-@pytest.mark.parametrize("name,steps", [("json", range(0, 60, 3)), ("schema", range(0, 1000, 50))])
+@pytest.mark.parametrize("name,steps", [("json", range(0, 60, 3)), ("schema", range(0, 1000, 50)),
+                                        ("pylike", range(0, 500, 100)), ("stress", range(0, 1000, 250))])
 def test_full_shape_steps_bit_exact(built, name, steps):
     """Every row of every listed step at the workload's full batch and
     vocabulary (the shape the benchmark times), one launch per step."""
@@ -151,7 +152,8 @@ def test_apply_matches_closed_form(B, V, dtype):
     assert (buf[B * V:].cpu() == 7).all()
 
 
-@pytest.mark.parametrize("name,step", [("arithmetic", 5), ("json", 7), ("schema", 3), ("schema", 777)])
+@pytest.mark.parametrize("name,step", [("arithmetic", 5), ("json", 7), ("schema", 3), ("schema", 777),
+                                       ("pylike", 11), ("stress", 13)])
 def test_apply_after_compute_end_to_end(built, name, step):
     """The whole step (compute_masks then apply_mask on one stream) against
     the oracle's masks applied by the closed form."""
