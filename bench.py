@@ -38,6 +38,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--warm-cache", action="store_true", help="single logits buffer (cache-resident; labelled)")
+    ap.add_argument("--calibration-copy-mb", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1 "
@@ -90,6 +92,18 @@ def main():
     n_bm = 4
     bms = [torch.empty((B, W), dtype=torch.int32, device=dev) for _ in range(n_bm)]
     log(f"logits pool {n_pool} x {per_buf / 1e6:.1f} MB")
+
+    if args.calibration_copy_mb:
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings
+        # give the counters' bytes-per-KiB scale on this GPU
+        n = args.calibration_copy_mb << 20
+        src_t = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst_t = torch.empty(n, dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            dst_t.copy_(src_t)
+        torch.cuda.synchronize()
+        del src_t, dst_t
+        log(f"calibration copy: 3 x {args.calibration_copy_mb} MiB device-to-device")
 
     def step(i):
         stacks, lens, qs = step_inputs[i % n_distinct]
@@ -154,38 +168,47 @@ def main():
         def only_apply(i):
             apply_mask(pool[i % n_pool], bms[i % n_bm], stream=stream)
 
+        t_apply = solo(only_apply)          # masks of steps 0..n_bm-1, as counted below
         t_compute = solo(only_compute)
-        t_apply = solo(only_apply)
 
-    # algorithmic bytes, from the actual masks of the distinct steps (the
-    # apply-only loop above used the masks of steps 0..n_bm-1)
-    zeros_total, stack_total = 0, 0
-    apply_zeros = []
+    # Algorithmic bytes of the in-place apply, from the actual masks: the
+    # bitmask is read once; a 16-byte vector of logits whose entries are all
+    # masked is written once (16 B); one that keeps some entries and masks
+    # others must be read to be written (32 B); one that keeps all entries is
+    # not touched.  (V % 32 == 0 here, so vectors never straddle rows.)
+    per_vec = 16 // s_logit
+    apply_bytes, stack_total = [], 0
     for s in range(n_distinct):
         stacks, lens, qs = step_inputs[s]
         clf.compute_masks(stacks, lens, qs, out=bms[0], stream=stream)
         torch.cuda.synchronize()
         m = bms[0].cpu().numpy().view(np.uint32)
-        ones = int(np.unpackbits(m.view(np.uint8), bitorder="little").sum())
-        zeros_total += B * V - ones
-        if s < n_bm:
-            apply_zeros.append(B * V - ones)
+        if per_vec == 8:
+            groups = m.view(np.uint8).reshape(-1)
+            full = 0xFF
+        else:
+            b8 = m.view(np.uint8).reshape(-1)
+            groups = np.stack([b8 & 0xF, b8 >> 4], axis=1).reshape(-1)
+            full = 0xF
+        n_masked = int((groups == 0).sum())
+        n_mixed = int(((groups != 0) & (groups != full)).sum())
+        apply_bytes.append(4 * W * B + 16 * n_masked + 32 * n_mixed)
         stack_total += int(lens.sum().item())
-    zeros_per_step = zeros_total / n_distinct
     stack_words = stack_total / n_distinct
     bytes_compute = 4 * stack_words + 8 * B + 2 * 4 * W * B         # stacks, lens+states, row read + write
-    bytes_apply = 4 * W * B + s_logit * zeros_per_step               # bitmask read + -inf writes
+    bytes_apply = float(np.mean(apply_bytes))
     bytes_step = bytes_compute + bytes_apply
     one_pass_model = B * (2 * V * s_logit + 3 * 4 * W) + 4 * (stack_words + 2 * B)
 
     lat_us = ms_per_step * 1e3
     masks_per_s = B / (ms_per_step * 1e-3)
-    bytes_apply_solo = 4 * W * B + s_logit * float(np.mean(apply_zeros))
+    bytes_apply_solo = float(np.mean(apply_bytes[:n_bm]))
     achieved_apply = bytes_apply_solo / (t_apply * 1e-6) / 1e9
     roofline = {
         "bound": "hbm", "kernel": "apply_fast_kernel" if V % 32 == 0 else "apply_generic_kernel",
         "achieved": round(achieved_apply, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved_apply / HBM_PEAK_GBS, 4), "traffic": None,
+        "frac": round(achieved_apply / HBM_PEAK_GBS, 4),
+        "traffic": measured_traffic(wl.name, "apply_fast_kernel") if V % 32 == 0 else None,
         "algorithmic_bytes_per_launch": round(bytes_apply_solo),
         "avg_launch_us": round(t_apply, 3),
         "timing": "HIP events around 1000 back-to-back launches of the kernel alone on the bench stream",
@@ -225,6 +248,26 @@ def main():
                                         "build_seconds", "dfa_rows", "dense_rows")},
     }
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
+    None when there is none for this workload or the kernel source changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{workload}_c3_pmc_traffic.md" if workload == "schema" else
+                        f"{workload}_pmc_traffic.md")
+    if not os.path.exists(path):
+        return None
+    meta = None
+    for line in open(path):
+        if line.startswith("traffic_json: "):
+            meta = json.loads(line[len("traffic_json: "):])
+    src = os.path.join(ROOT, "paper_2608_03065_amd", "csrc", "psc_device.hip")
+    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if not meta or meta.get("source_sha256_16") != h or kernel not in meta.get("kernels", {}):
+        return None
+    return meta["kernels"][kernel]["hbm_bytes"]
 
 
 def cpu_baseline(wl, step_states, seconds, B):
