@@ -1,9 +1,11 @@
 #!/usr/bin/env python3
 """Per-step mask + apply benchmark on one MI355X.
 
-A step is one pass of the whole hot path over one batch: psc_compute_masks
-(classifier walk + mask-row gather) followed by psc_apply_mask (in-place
--inf on the logits), both on one stream, inputs already resident in HBM.
+A step is one pass of the whole hot path over one batch, inputs already
+resident in HBM: the classifier walk, the gather of each class's mask row
+into the bitmask, and the in-place -inf on the logits.  By default it is one
+psc_compute_and_apply launch; --mode two-launch times psc_compute_masks
+followed by psc_apply_mask on the same stream instead.
 Prints ONE JSON line (see the field list at the bottom).
 """
 from __future__ import annotations
@@ -33,6 +35,9 @@ def main():
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="schema")
+    ap.add_argument("--mode", choices=["fused", "two-launch"], default="fused",
+                    help="fused: psc_compute_and_apply (one launch); two-launch: psc_compute_masks + "
+                         "psc_apply_mask")
     ap.add_argument("--distinct-steps", type=int, default=None,
                     help="distinct prefix batches generated (default: the workload's step count)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -105,58 +110,43 @@ def main():
         del src_t, dst_t
         log(f"calibration copy: 3 x {args.calibration_copy_mb} MiB device-to-device")
 
-    def step(i):
+    def fused_step(i):
+        stacks, lens, qs = step_inputs[i % n_distinct]
+        clf.compute_and_apply(stacks, lens, qs, pool[i % n_pool], out=bms[i % n_bm], stream=stream)
+
+    def two_launch_step(i):
         stacks, lens, qs = step_inputs[i % n_distinct]
         bm = bms[i % n_bm]
         clf.compute_masks(stacks, lens, qs, out=bm, stream=stream)
         apply_mask(pool[i % n_pool], bm, stream=stream)
+
+    step = fused_step if args.mode == "fused" else two_launch_step
+    other = two_launch_step if args.mode == "fused" else fused_step
+
+    def loop(fn, n, warm=20):
+        """HIP events on the bench stream around n back-to-back calls."""
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for i in range(warm):
+            fn(i)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(n):
+            fn(i)
+        z.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / n * 1e3     # us per call
 
     with torch.cuda.stream(stream):
         for i in range(args.warmup):
             step(i)
         torch.cuda.synchronize()
 
-        # (1) clean timed loop: whole-step latency
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        start.record(stream)
-        for i in range(args.steps):
-            step(i)
-        end.record(stream)
-        torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
-        ms_per_step = total_ms / args.steps
+        # (1) the timed loop: exactly --steps steps, whole-step latency
+        ms_per_step = loop(step, args.steps, warm=0) * 1e-3
+        # (2) the other formulation of the same step, for comparison
+        t_other = loop(other, min(args.steps, 1000))
 
-        # (2) per-kernel durations with events around each launch
-        K = min(args.steps, 1000)
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
-        torch.cuda.synchronize()
-        for i in range(K):
-            stacks, lens, qs = step_inputs[i % n_distinct]
-            bm = bms[i % n_bm]
-            ev[i][0].record(stream)
-            clf.compute_masks(stacks, lens, qs, out=bm, stream=stream)
-            ev[i][1].record(stream)
-            apply_mask(pool[i % n_pool], bm, stream=stream)
-            ev[i][2].record(stream)
-        torch.cuda.synchronize()
-        t_compute_ev = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) * 1e3   # us
-        t_apply_ev = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
-
-        # (3) each kernel alone, back to back on the stream: the average launch
-        # duration (events over the whole loop, no per-launch markers)
-        def solo(fn, n=1000):
-            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            for i in range(20):
-                fn(i)
-            torch.cuda.synchronize()
-            a.record(stream)
-            for i in range(n):
-                fn(i)
-            z.record(stream)
-            torch.cuda.synchronize()
-            return a.elapsed_time(z) / n * 1e3
-
+        # (3) each kernel of the two-launch step alone, back to back
         def only_compute(i):
             stacks, lens, qs = step_inputs[i % n_distinct]
             clf.compute_masks(stacks, lens, qs, out=bms[i % n_bm], stream=stream)
@@ -168,16 +158,18 @@ def main():
         def only_apply(i):
             apply_mask(pool[i % n_pool], bms[i % n_bm], stream=stream)
 
-        t_apply = solo(only_apply)          # masks of steps 0..n_bm-1, as counted below
-        t_compute = solo(only_compute)
+        t_apply = loop(only_apply, 1000)     # masks of steps 0..n_bm-1, as counted below
+        t_compute = loop(only_compute, 1000)
 
-    # Algorithmic bytes of the in-place apply, from the actual masks: the
-    # bitmask is read once; a 16-byte vector of logits whose entries are all
-    # masked is written once (16 B); one that keeps some entries and masks
-    # others must be read to be written (32 B); one that keeps all entries is
-    # not touched.  (V % 32 == 0 here, so vectors never straddle rows.)
+    # Algorithmic bytes, from the actual masks.  The apply touches logits per
+    # 16-byte vector: one whose entries are all masked is written once
+    # (16 B); one that keeps some entries and masks others must be read to be
+    # written (32 B); one that keeps all entries is not touched.  (V % 32 == 0
+    # here, so vectors never straddle rows.)  The walk reads the stacks, lens
+    # and states; the gather reads the class's mask row and writes the
+    # bitmask (4 W B each); the two-launch apply reads the bitmask back.
     per_vec = 16 // s_logit
-    apply_bytes, stack_total = [], 0
+    logit_bytes, stack_total = [], 0
     for s in range(n_distinct):
         stacks, lens, qs = step_inputs[s]
         clf.compute_masks(stacks, lens, qs, out=bms[0], stream=stream)
@@ -192,27 +184,43 @@ def main():
             full = 0xF
         n_masked = int((groups == 0).sum())
         n_mixed = int(((groups != 0) & (groups != full)).sum())
-        apply_bytes.append(4 * W * B + 16 * n_masked + 32 * n_mixed)
+        logit_bytes.append(16 * n_masked + 32 * n_mixed)
         stack_total += int(lens.sum().item())
     stack_words = stack_total / n_distinct
-    bytes_compute = 4 * stack_words + 8 * B + 2 * 4 * W * B         # stacks, lens+states, row read + write
-    bytes_apply = float(np.mean(apply_bytes))
-    bytes_step = bytes_compute + bytes_apply
+    bytes_walk_gather = 4 * stack_words + 8 * B + 2 * 4 * W * B
+    bytes_fused = bytes_walk_gather + float(np.mean(logit_bytes))
+    bytes_two_launch = bytes_fused + 4 * W * B
+    bytes_step = bytes_fused if args.mode == "fused" else bytes_two_launch
     one_pass_model = B * (2 * V * s_logit + 3 * 4 * W) + 4 * (stack_words + 2 * B)
 
     lat_us = ms_per_step * 1e3
     masks_per_s = B / (ms_per_step * 1e-3)
-    bytes_apply_solo = float(np.mean(apply_bytes[:n_bm]))
+    bytes_apply_solo = 4 * W * B + float(np.mean(logit_bytes[:n_bm]))
     achieved_apply = bytes_apply_solo / (t_apply * 1e-6) / 1e9
-    roofline = {
-        "bound": "hbm", "kernel": "apply_fast_kernel" if V % 32 == 0 else "apply_generic_kernel",
-        "achieved": round(achieved_apply, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved_apply / HBM_PEAK_GBS, 4),
-        "traffic": measured_traffic(wl.name, "apply_fast_kernel") if V % 32 == 0 else None,
-        "algorithmic_bytes_per_launch": round(bytes_apply_solo),
-        "avg_launch_us": round(t_apply, 3),
-        "timing": "HIP events around 1000 back-to-back launches of the kernel alone on the bench stream",
-    }
+    fast = V % 32 == 0
+    if args.mode == "fused":
+        kname = "fused_fast_kernel" if fast else "fused_generic_kernel"
+        achieved = bytes_fused / (lat_us * 1e-6) / 1e9
+        roofline = {
+            "bound": "hbm", "kernel": kname,
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(wl.name, kname) if fast else None,
+            "algorithmic_bytes_per_launch": round(bytes_fused),
+            "avg_launch_us": round(lat_us, 3),
+            "timing": "HIP events on the bench stream around the timed loop; one launch per step",
+        }
+    else:
+        kname = "apply_fast_kernel" if fast else "apply_generic_kernel"
+        roofline = {
+            "bound": "hbm", "kernel": kname,
+            "achieved": round(achieved_apply, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved_apply / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(wl.name, kname) if fast else None,
+            "algorithmic_bytes_per_launch": round(bytes_apply_solo),
+            "avg_launch_us": round(t_apply, 3),
+            "timing": "HIP events around 1000 back-to-back launches of the kernel alone on the bench stream",
+        }
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -238,10 +246,13 @@ def main():
             "B": B, "V": V, "logits": wl.logits_dtype, "distinct_steps": n_distinct,
             "logits_pool_buffers": n_pool, "warm_cache": bool(args.warm_cache),
         },
+        "step_mode": args.mode,
+        "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
-                       "compute_masks_in_step_events": round(t_compute_ev, 3),
-                       "apply_mask_in_step_events": round(t_apply_ev, 3)},
-        "bytes_per_step": {"algorithmic": round(bytes_step), "one_pass_read_write_model": round(one_pass_model)},
+                       "apply_mask_solo_gbs": round(achieved_apply, 1)},
+        "bytes_per_step": {"algorithmic": round(bytes_step), "fused": round(bytes_fused),
+                           "two_launch": round(bytes_two_launch),
+                           "one_pass_read_write_model": round(one_pass_model)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "build": {k: info[k] for k in ("dfa_states", "n_classes", "table_bytes", "mask_table_bytes",

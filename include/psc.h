@@ -169,6 +169,26 @@ psc_status psc_compute_masks(const psc_handle *h, const int32_t *stacks, const i
 psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask, int32_t B,
                           int32_t V, void *stream);
 
+/*
+ * The whole per-step path in one launch: psc_compute_masks followed by
+ * psc_apply_mask (Algorithm 2, classification and mask steps; Sec. 1,
+ * Fig. 1a), fused so that each workgroup walks its sequence, gathers its
+ * slice of the class's mask row and applies it to the logits directly.
+ *  stacks, stack_lens, lexer_states  as for psc_compute_masks.
+ *  out_bitmask  device uint32 [B][W], fully written as by psc_compute_masks;
+ *               may be NULL when only the masked logits are wanted.
+ *  logits       device, contiguous [B][V] of `dtype`, masked in place as by
+ *               psc_apply_mask; V must equal the vocabulary size of `h`.
+ * A rejected sequence (see psc_compute_masks) gets an all-zero mask row, so
+ * its whole logits row becomes -inf, and counts once in the error counter.
+ * Results are bit-identical to the two separate calls.  B == 0 is a no-op.
+ * Errors: PSC_E_INVALID_ARG (also V != vocabulary size), PSC_E_NOT_BOUND,
+ * PSC_E_DEVICE.
+ */
+psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                 const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
+                                 psc_dtype dtype, int32_t V, void *stream);
+
 /* Read (synchronously, on `stream`) and optionally reset the device counter
  * of sequences that psc_compute_masks rejected as out of range. */
 psc_status psc_device_error_count(const psc_handle *h, uint32_t *out, int32_t reset, void *stream);

@@ -39,15 +39,10 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
     return make_uint4(x.x, x.y, x.z, x.w);
 }
 
-// One workgroup per (sequence b, slice of the mask row).  Wavefront 0 walks
-// the classifier for sequence b (every slice of the same b repeats the walk,
-// which costs latency but no bandwidth), then the whole workgroup copies its
-// slice of the class's precomputed mask row into out_bitmask[b].
-//
-// Walk (Algorithm 2, classification step): ref = start[q]; read the stack
-// top-first; stop as soon as ref names a class (a determined state).  The
-// walk is a chain of dependent loads, so every step is exactly ONE
-// wavefront-wide vector load of the current row:
+// Walk of sequence b by one wavefront (Algorithm 2, classification step):
+// ref = start[q]; read the stack top-first; stop as soon as ref names a
+// class (a determined state).  The walk is a chain of dependent loads, so
+// every step is exactly ONE wavefront-wide vector load of the current row:
 //   sparse row: lane 0 <- (end_class, n_edges), lane 1 <- (default, skip),
 //               lane j >= 2 <- edge j-2 as (symbol, ref); the edge matching
 //               the symbol is found with a ballot and read with readlane;
@@ -57,98 +52,118 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
 // Before the walk: round trip 1 fetches lens[b], qs[b] and the lengths before
 // b (start offset); round trip 2 fetches the top kChunk stack symbols (lane j
 // holds the j-th symbol below the chunk's top) together with start[q] in
-// lane 63.
+// lane 63.  Returns the class id, or -1 for a rejected input (length <= 0,
+// lexer state or stack symbol out of range); the result is wave-uniform.
 constexpr int kChunk = kWave - 1;
 static_assert(kSparseMax <= kWave - 2, "a sparse row must fit one wavefront load");
 
+__device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
+                                          const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
+                                          const int32_t *__restrict__ qs, int b, int lane) {
+    // round trip 1 (all independent; vector loads so no scalar load queues
+    // behind the reduction)
+    const int own = *((lane & 1) ? qs + b : lens + b);
+    int part = lane < b ? lens[lane] : 0;
+    for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+    const int len = __builtin_amdgcn_readlane(own, 0);
+    const int q = __builtin_amdgcn_readlane(own, 1);
+    const int off = wave_sum(part);
+    int cls = -1;   // -1 = rejected input
+    if (len > 0 && q >= 0 && q < n_lex) {
+        const int32_t *st = stacks + off;
+        int i = len - 1;           // index of the next symbol to read
+        int chunk_base = i;        // stack index held by lane 0
+        // round trip 2: stack chunk + start[q]
+        const int32_t *a0 = lane == kChunk ? table + q
+                          : (chunk_base - lane >= 0 ? st + (chunk_base - lane) : table + q);
+        int sym = *a0;
+        int ref = __builtin_amdgcn_readlane(sym, kChunk);
+        for (;;) {
+            if (ref < 0) { cls = -ref - 1; break; }
+            if (i >= 0 && chunk_base - i >= kChunk) {
+                chunk_base = i;
+                sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
+            }
+            const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+            const bool x_ok = X >= 0 && X < n_lr;
+            const int32_t *row = table + (ref & ~1);
+            const bool dense = ref & 1;
+            // the one load of this step: one aligned 8-byte load per lane
+            // (a dense row's lane 1 takes the aligned pair holding entry X)
+            const int Xc = x_ok ? X : 0;
+            const int ia = dense ? (lane == 0 ? 0 : kRowHeader + (Xc & ~1)) : 2 * lane;
+            const int2 v = *reinterpret_cast<const int2 *>(row + ia);
+            const int va = v.x, vc = v.y;
+            if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); break; }
+            if (dense) {
+                if (!x_ok) break;
+                ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
+                i--;
+                continue;
+            }
+            const int n = __builtin_amdgcn_readlane(vc, 0);
+            if (n == 0) {                                    // skip chain
+                const int L = max(__builtin_amdgcn_readlane(vc, 1), 1);   // >= 1: always progresses
+                const int t = min(L, i + 1);
+                int left = t;
+                bool bad = false;
+                while (left > 0) {
+                    if (chunk_base - i >= kChunk) {
+                        chunk_base = i;
+                        sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
+                    }
+                    const int pos = chunk_base - i;
+                    const int take = min(left, kChunk - pos);
+                    bad |= __ballot(lane >= pos && lane < pos + take && (sym < 0 || sym >= n_lr)) != 0;
+                    i -= take;
+                    left -= take;
+                }
+                if (bad) break;
+                if (t < L) { cls = __builtin_amdgcn_readlane(va, 0); break; }
+                ref = __builtin_amdgcn_readlane(va, 1);
+                continue;
+            }
+            if (!x_ok) break;
+            const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
+            ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
+                      : __builtin_amdgcn_readlane(va, 1);
+            i--;
+        }
+    }
+    return cls;
+}
+
+// Wavefront 0 of the workgroup walks sequence b; the class (or -1) is
+// published to the whole workgroup through LDS.  Slice 0 of each sequence
+// counts rejected inputs.
+__device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
+                                           const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
+                                           const int32_t *__restrict__ qs, int b, uint32_t *__restrict__ err) {
+    __shared__ int32_t s_cls;
+    if (threadIdx.x < kWave) {
+        const int cls = walk_class(table, n_lex, n_lr, stacks, lens, qs, b, threadIdx.x);
+        if (threadIdx.x == 0) {
+            s_cls = cls;
+            if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
+        }
+    }
+    __syncthreads();
+    return s_cls;
+}
+
+// One workgroup per (sequence b, slice of the mask row): the walk, then the
+// whole workgroup copies its slice of the class's precomputed mask row into
+// out_bitmask[b] (Algorithm 2, mask step).  Every slice of the same b repeats
+// the walk, which costs latency but no HBM bandwidth (the rows are cached).
 __global__ void __launch_bounds__(kBlock)
 walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks,
                    int32_t mask_stride, int32_t n_lex, int32_t n_lr,
                    const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
                    const int32_t *__restrict__ qs, int32_t B, int32_t W,
                    uint32_t *__restrict__ out, uint32_t *__restrict__ err, int32_t vec4) {
-    __shared__ int32_t s_cls;
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
-    if (tid < kWave) {
-        const int lane = tid;
-        // round trip 1 (all independent; vector loads so no scalar load
-        // queues behind the reduction)
-        const int own = *((lane & 1) ? qs + b : lens + b);
-        int part = lane < b ? lens[lane] : 0;
-        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
-        const int len = __builtin_amdgcn_readlane(own, 0);
-        const int q = __builtin_amdgcn_readlane(own, 1);
-        const int off = wave_sum(part);
-        int cls = -1;   // -1 = fault
-        if (len > 0 && q >= 0 && q < n_lex) {
-            const int32_t *st = stacks + off;
-            int i = len - 1;           // index of the next symbol to read
-            int chunk_base = i;        // stack index held by lane 0
-            // round trip 2: stack chunk + start[q]
-            const int32_t *a0 = lane == kChunk ? table + q
-                              : (chunk_base - lane >= 0 ? st + (chunk_base - lane) : table + q);
-            int sym = *a0;
-            int ref = __builtin_amdgcn_readlane(sym, kChunk);
-            for (;;) {
-                if (ref < 0) { cls = -ref - 1; break; }
-                if (i >= 0 && chunk_base - i >= kChunk) {
-                    chunk_base = i;
-                    sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
-                }
-                const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
-                const bool x_ok = X >= 0 && X < n_lr;
-                const int32_t *row = table + (ref & ~1);
-                const bool dense = ref & 1;
-                // the one load of this step: one aligned 8-byte load per lane
-                // (a dense row's lane 1 takes the aligned pair holding entry X)
-                const int Xc = x_ok ? X : 0;
-                const int ia = dense ? (lane == 0 ? 0 : kRowHeader + (Xc & ~1)) : 2 * lane;
-                const int2 v = *reinterpret_cast<const int2 *>(row + ia);
-                const int va = v.x, vc = v.y;
-                if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); break; }
-                if (dense) {
-                    if (!x_ok) break;
-                    ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
-                    i--;
-                    continue;
-                }
-                const int n = __builtin_amdgcn_readlane(vc, 0);
-                if (n == 0) {                                    // skip chain
-                    const int L = max(__builtin_amdgcn_readlane(vc, 1), 1);   // >= 1: always progresses
-                    const int t = min(L, i + 1);
-                    int left = t;
-                    bool bad = false;
-                    while (left > 0) {
-                        if (chunk_base - i >= kChunk) {
-                            chunk_base = i;
-                            sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
-                        }
-                        const int pos = chunk_base - i;
-                        const int take = min(left, kChunk - pos);
-                        bad |= __ballot(lane >= pos && lane < pos + take && (sym < 0 || sym >= n_lr)) != 0;
-                        i -= take;
-                        left -= take;
-                    }
-                    if (bad) break;
-                    if (t < L) { cls = __builtin_amdgcn_readlane(va, 0); break; }
-                    ref = __builtin_amdgcn_readlane(va, 1);
-                    continue;
-                }
-                if (!x_ok) break;
-                const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
-                ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
-                          : __builtin_amdgcn_readlane(va, 1);
-                i--;
-            }
-        }
-        if (lane == 0) {
-            s_cls = cls;
-            if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
-        }
-    }
-    __syncthreads();
-    const int cls = s_cls;
+    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
     const int w0 = blockIdx.x * kCopyWordsPerBlock;
     const int w1 = min(W, w0 + kCopyWordsPerBlock);
     uint32_t *dst = out + (size_t)b * W;
@@ -172,42 +187,41 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
 constexpr uint16_t kBf16NegInf = 0xFF80u;
 constexpr uint32_t kF32NegInf = 0xFF800000u;
 
-// Fast path: V % 32 == 0 and 16-byte aligned logits, so the flat element
-// index is exactly 32 x the flat mask-word index and rows never split a
-// vector.  Each wavefront owns 64 (bf16) or 32 (fp32) consecutive mask words
-// and writes them as kVecs contiguous 1 KiB vector stores; lanes get their 8 (bf16) or
-// 4 (fp32) mask bits from the owning lane by a cross-lane shuffle.  Entries
-// whose bit is set are never touched: an all-zero group is one store of
-// -inf, a mixed group is a read-select-write of that 16-byte vector only
-// (all of a lane's reads are issued before its stores).
+// One wavefront applies kWordsPerWave consecutive mask words to the logits
+// they cover (the row length V is a multiple of 32 and the logits are 16-byte
+// aligned, so word w covers exactly the 32 elements at 32*w).  Lane j holds
+// word j in `m` (all ones past the end: nothing to do).  The wavefront writes
+// its 64 (bf16) or 32 (fp32) words as kVecs contiguous 1 KiB vector stores;
+// lanes get their 8 (bf16) or 4 (fp32) mask bits from the owning lane by a
+// cross-lane shuffle.  Entries whose bit is set are never touched: an
+// all-zero group is one store of -inf, a mixed group is a read-select-write
+// of that 16-byte vector only (all of a lane's reads are issued before its
+// stores).
 template <bool kBf16>
-__global__ void __launch_bounds__(kBlock)
-apply_fast_kernel(uint4 *__restrict__ logits, const uint32_t *__restrict__ bits, int64_t n_words) {
-    constexpr int kPerVec = kBf16 ? 8 : 4;          // elements per 16-byte vector
-    constexpr int kVecsPerWord = 32 / kPerVec;
-    constexpr int kVecs = 4;                        // vectors per lane
-    constexpr int kWordsPerWave = kWave * kVecs / kVecsPerWord;
-    constexpr uint32_t kFull = (1u << kPerVec) - 1;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
-    const int64_t w_base = wave * kWordsPerWave;
-    if (w_base >= n_words) return;
-    uint32_t m = 0xFFFFFFFFu;                       // words past the end: nothing to do
-    if (lane < kWordsPerWave && w_base + lane < n_words) m = bits[w_base + lane];
-    uint4 *base = logits + w_base * kVecsPerWord;
-    uint32_t g[kVecs];
-    uint4 x[kVecs];
+struct ApplyGeom {
+    static constexpr int kPerVec = kBf16 ? 8 : 4;           // elements per 16-byte vector
+    static constexpr int kVecsPerWord = 32 / kPerVec;
+    static constexpr int kVecs = 4;                         // vectors per lane
+    static constexpr int kWordsPerWave = kWave * kVecs / kVecsPerWord;
+};
+
+template <bool kBf16>
+__device__ __forceinline__ void apply_words(uint4 *__restrict__ base, uint32_t m, int lane) {
+    using G = ApplyGeom<kBf16>;
+    constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
+    uint32_t g[G::kVecs];
+    uint4 x[G::kVecs];
 #pragma unroll
-    for (int j = 0; j < kVecs; j++) {
+    for (int j = 0; j < G::kVecs; j++) {
         // vector v = j*64 + lane covers elements [kPerVec*v, kPerVec*v + kPerVec)
         const int v = j * kWave + lane;
-        g[j] = (__shfl(m, v / kVecsPerWord, kWave) >> ((v % kVecsPerWord) * kPerVec)) & kFull;
+        g[j] = (__shfl(m, v / G::kVecsPerWord, kWave) >> ((v % G::kVecsPerWord) * G::kPerVec)) & kFull;
     }
 #pragma unroll
-    for (int j = 0; j < kVecs; j++)
+    for (int j = 0; j < G::kVecs; j++)
         if (g[j] != 0 && g[j] != kFull) x[j] = load_nt(base + j * kWave + lane);
 #pragma unroll
-    for (int j = 0; j < kVecs; j++) {
+    for (int j = 0; j < G::kVecs; j++) {
         if (g[j] == kFull) continue;
         uint4 val;
         if (g[j] == 0) {
@@ -233,6 +247,21 @@ apply_fast_kernel(uint4 *__restrict__ logits, const uint32_t *__restrict__ bits,
     }
 }
 
+// Fast path of psc_apply_mask: the B rows are one flat run of n_words mask
+// words (V % 32 == 0), split over wavefronts.
+template <bool kBf16>
+__global__ void __launch_bounds__(kBlock)
+apply_fast_kernel(uint4 *__restrict__ logits, const uint32_t *__restrict__ bits, int64_t n_words) {
+    using G = ApplyGeom<kBf16>;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    const int64_t w_base = wave * G::kWordsPerWave;
+    if (w_base >= n_words) return;
+    uint32_t m = 0xFFFFFFFFu;
+    if (lane < G::kWordsPerWave && w_base + lane < n_words) m = bits[w_base + lane];
+    apply_words<kBf16>(logits + w_base * G::kVecsPerWord, m, lane);
+}
+
 // General path: any V and alignment, one element per thread.
 template <bool kBf16>
 __global__ void __launch_bounds__(kBlock)
@@ -244,6 +273,67 @@ apply_generic_kernel(void *__restrict__ logits, const uint32_t *__restrict__ bit
         if ((bits[b * W + (v >> 5)] >> (v & 31)) & 1u) continue;
         if (kBf16) reinterpret_cast<uint16_t *>(logits)[e] = kBf16NegInf;
         else reinterpret_cast<uint32_t *>(logits)[e] = kF32NegInf;
+    }
+}
+
+// ---------------------------------------------------------------- fused step
+
+// psc_compute_and_apply, fast path (V % 32 == 0, 16-byte aligned logits):
+// one workgroup per (sequence b, slice of kBlock / kWave * kWordsPerWave mask
+// words).  After the walk, every wavefront loads its words of the class's
+// mask row once, writes them to out_bitmask[b] (when requested) and applies
+// them to logits[b] in place.  One launch instead of two, and the bitmask is
+// not read back from HBM between the gather and the apply.
+template <bool kBf16>
+__global__ void __launch_bounds__(kBlock)
+fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                  const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
+                  uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
+    using G = ApplyGeom<kBf16>;
+    const int b = blockIdx.y;
+    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w_base = (blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * G::kWordsPerWave;
+    if (w_base >= W) return;
+    uint32_t m = 0xFFFFFFFFu;
+    const int w = w_base + lane;
+    if (lane < G::kWordsPerWave && w < W) {
+        m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w];
+        if (out) out[(size_t)b * W + w] = m;
+    }
+    apply_words<kBf16>(logits + ((size_t)b * W + w_base) * G::kVecsPerWord, m, lane);
+}
+
+// psc_compute_and_apply, general path (any V, any element alignment): one
+// workgroup per (sequence b, kGenWords mask words); the words go through LDS
+// and each thread then masks single elements.
+constexpr int kGenWords = 128;
+static_assert(kGenWords <= kBlock, "one pass stages the slice's words");
+
+template <bool kBf16>
+__global__ void __launch_bounds__(kBlock)
+fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                     const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
+                     uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
+    __shared__ uint32_t s_m[kGenWords];
+    const int b = blockIdx.y;
+    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
+    const int w0 = blockIdx.x * kGenWords;
+    const int nw = min(kGenWords, W - w0);
+    if (threadIdx.x < nw) {
+        const uint32_t m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w0 + threadIdx.x];
+        s_m[threadIdx.x] = m;
+        if (out) out[(size_t)b * W + w0 + threadIdx.x] = m;
+    }
+    __syncthreads();
+    const int e0 = w0 * 32, e1 = min(V, (w0 + nw) * 32);
+    for (int e = e0 + threadIdx.x; e < e1; e += kBlock) {
+        if ((s_m[(e - e0) >> 5] >> (e & 31)) & 1u) continue;
+        const size_t idx = (size_t)b * V + e;
+        if (kBf16) reinterpret_cast<uint16_t *>(logits)[idx] = kBf16NegInf;
+        else reinterpret_cast<uint32_t *>(logits)[idx] = kF32NegInf;
     }
 }
 
@@ -369,4 +459,60 @@ extern "C" psc_status psc_device_error_count(const psc_handle *h, uint32_t *out,
     if (e == hipSuccess && reset) e = hipMemsetAsync(h->dev_base, 0, sizeof(uint32_t), s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     return e == hipSuccess ? PSC_OK : device_fail("psc_device_error_count", e);
+}
+
+extern "C" psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                            const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
+                                            void *logits, psc_dtype dtype, int32_t V, void *stream) {
+    if (!h || B < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
+        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits))) {
+        set_error("psc_compute_and_apply: null argument, B < 0 or bad dtype");
+        return PSC_E_INVALID_ARG;
+    }
+    if (V != h->V) {
+        set_error("psc_compute_and_apply: V (" + std::to_string(V) + ") differs from the vocabulary size (" +
+                  std::to_string(h->V) + ")");
+        return PSC_E_INVALID_ARG;
+    }
+    if (!h->dev_base) {
+        set_error("psc_compute_and_apply: device tables not bound");
+        return PSC_E_NOT_BOUND;
+    }
+    if (B > 65535) {
+        set_error("psc_compute_and_apply: B > 65535");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(h->dev_base);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
+    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const int32_t W = h->W;
+    const bool bf16 = dtype == PSC_BF16;
+    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    if (fast) {
+        const int words_per_block = (kBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
+                                                             : ApplyGeom<false>::kWordsPerWave);
+        dim3 grid((W + words_per_block - 1) / words_per_block, B);
+        if (bf16)
+            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, W, out_bitmask, err,
+                               reinterpret_cast<uint4 *>(logits));
+        else
+            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, W, out_bitmask, err,
+                               reinterpret_cast<uint4 *>(logits));
+    } else {
+        dim3 grid((W + kGenWords - 1) / kGenWords, B);
+        if (bf16)
+            hipLaunchKernelGGL(fused_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, V, W, out_bitmask, err, logits);
+        else
+            hipLaunchKernelGGL(fused_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
+                               h->mask_stride, h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, V, W,
+                               out_bitmask, err, logits);
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail("psc_compute_and_apply", e);
 }

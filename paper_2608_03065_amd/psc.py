@@ -19,7 +19,7 @@ _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E
            -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT"}
 
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
-            "psc_apply_mask", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_apply_mask", "psc_compute_and_apply", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -76,6 +76,7 @@ def lib() -> C.CDLL:
         L.psc_bind_device.argtypes = [P, P, C.c_size_t, P]
         L.psc_compute_masks.argtypes = [P, P, P, P, I32, P, P]
         L.psc_apply_mask.argtypes = [P, C.c_int, P, I32, I32, P]
+        L.psc_compute_and_apply.argtypes = [P, P, P, P, I32, P, P, C.c_int, I32, P]
         L.psc_device_error_count.argtypes = [P, P, I32, P]
         L.psc_classify_host.argtypes = [P, P, P, P, I32, P]
         L.psc_class_mask_host.argtypes = [P, I32, P]
@@ -83,7 +84,7 @@ def lib() -> C.CDLL:
         L.psc_free.restype = None
         L.psc_last_error.restype = C.c_char_p
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
-                     "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
+                     "psc_compute_and_apply", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -202,6 +203,24 @@ class Classifier:
         _check(lib().psc_compute_masks(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
                                        lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
+
+    def compute_and_apply(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
+        """One launch: masks for the B prefix states applied to logits [B, V] in
+        place; the bitmask is also written to `out` when given.  Returns logits."""
+        import torch
+        B = int(stack_lens.shape[0])
+        for t in (stacks, stack_lens, lexer_states):
+            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
+        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (B, self.V)
+        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        out_ptr = None
+        if out is not None:
+            assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and tuple(out.shape) == (B, self.W)
+            out_ptr = out.data_ptr()
+        _check(lib().psc_compute_and_apply(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
+                                           lexer_states.data_ptr(), B, out_ptr, logits.data_ptr(), dt,
+                                           self.V, _stream_ptr(stream)))
+        return logits
 
     def error_count(self, reset: bool = False, stream=None) -> int:
         v = C.c_uint32()

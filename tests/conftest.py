@@ -34,3 +34,21 @@ def arith():
 @pytest.fixture(scope="session")
 def json_g():
     return grammar("json")
+
+
+@pytest.fixture(scope="session")
+def built():
+    """name -> (workload, device-bound Classifier, Oracle), built once per
+    session and shared by the GPU modules (the larger builds take minutes)."""
+    cache = {}
+
+    def get(name):
+        if name not in cache:
+            from inputs import configs
+            from oracle import Oracle
+            from paper_2608_03065_amd.psc import Classifier
+            wl = configs.get(name)
+            clf = Classifier(wl.grammar, wl.vocab).bind("cuda:0")
+            cache[name] = (wl, clf, Oracle(wl.grammar, wl.vocab))
+        return cache[name]
+    return get

@@ -5,10 +5,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
-from inputs import configs  # noqa: E402
-from oracle import Oracle  # noqa: E402
-from paper_2608_03065_amd import psc  # noqa: E402
-from paper_2608_03065_amd.psc import Classifier, apply_mask, pack_states  # noqa: E402
+from paper_2608_03065_amd.psc import apply_mask, pack_states  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -19,19 +16,6 @@ def _device_masks(clf, states):
     out = clf.compute_masks(stacks, lens, qs)
     torch.cuda.synchronize()
     return out.cpu().numpy().view(np.uint32)
-
-
-@pytest.fixture(scope="module")
-def built():
-    cache = {}
-
-    def get(name):
-        if name not in cache:
-            wl = configs.get(name)
-            clf = Classifier(wl.grammar, wl.vocab).bind(DEV)
-            cache[name] = (wl, clf, Oracle(wl.grammar, wl.vocab))
-        return cache[name]
-    return get
 
 
 def test_arithmetic_all_steps_bit_exact(built):
