@@ -100,13 +100,15 @@ typedef struct {
     int32_t n_classes;         /* distinct precomputed masks (rows)           */
     int64_t dfa_states_built;  /* automaton states before minimisation        */
     int32_t dfa_states;        /* after minimisation                          */
-    int32_t dfa_rows;          /* states that need a row (not determined)     */
+    int32_t dfa_rows;          /* states walked (not determined)              */
     int32_t dense_rows;        /* rows stored densely over Pi                 */
     int32_t max_sparse_edges;  /* largest sparse row                          */
     int64_t table_bytes;       /* classifier table bytes on the device        */
     int64_t mask_table_bytes;  /* mask table bytes on the device              */
     int64_t device_bytes;      /* total device buffer needed (psc_device_bytes) */
     double build_seconds;      /* wall time of psc_build                      */
+    int32_t chain_states;      /* walked states stored as chain entries       */
+    int32_t chains;            /* chains they form                            */
 } psc_info_t;
 
 /*

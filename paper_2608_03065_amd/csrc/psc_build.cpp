@@ -1077,61 +1077,93 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         h->n_lr = G.nPi;
         h->n_classes = (int32_t)kept.size();
         std::vector<int32_t> ref(nb, 0);
-        int64_t off = G.nQ + (G.nQ & 1);
-        int32_t rows = 0, dense = 0, max_sparse = 0;
+        // Thin states (at most two explicit edges) become chain entries.  A
+        // thin state moves on along its lowest explicit edge into a thin
+        // state, else along its lowest explicit edge, and an edge-free state
+        // along its default; chains follow these moves in canonical order.
+        const bool use_chains = G.nPi <= kMaxChainAlphabet;
+        auto is_thin = [&](int32_t b) { return use_chains && det[b] < 0 && m_ebeg[b + 1] - m_ebeg[b] <= 2; };
+        auto cont_edge = [&](int32_t b) -> int32_t {     // edge index, or -1: any symbol (default)
+            if (m_ebeg[b + 1] == m_ebeg[b]) return -1;
+            for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++)
+                if (is_thin(m_tgt[e])) return e;
+            return m_ebeg[b];
+        };
+        auto cont_target = [&](int32_t b) { int32_t e = cont_edge(b); return e < 0 ? m_def[b] : m_tgt[e]; };
+        std::vector<std::vector<int32_t>> chains;
+        {
+            std::vector<uint8_t> placed(nb, 0);
+            for (int32_t b : order) {
+                if (!is_thin(b) || placed[b]) continue;
+                std::vector<int32_t> ch{b};
+                placed[b] = 1;
+                for (int32_t t = cont_target(b); (int)ch.size() < kChainMax && is_thin(t) && !placed[t];
+                     t = cont_target(t)) {
+                    ch.push_back(t);
+                    placed[t] = 1;
+                }
+                chains.push_back(std::move(ch));
+            }
+        }
+        int64_t off = (G.nQ + 3) & ~3;
+        int32_t rows = 0, dense = 0, max_sparse = 0, chain_states = 0;
         for (int32_t b : order) {
             if (det[b] >= 0) { ref[b] = class_ref(det[b]); continue; }
+            rows++;
+            if (is_thin(b)) continue;
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             bool is_dense = ne > kSparseMax;
-            ref[b] = (int32_t)off | (is_dense ? 1 : 0);
+            ref[b] = (int32_t)off | (is_dense ? kRefDense : 0);
             int64_t len = kRowHeader + (is_dense ? (int64_t)G.nPi : 2LL * ne);
-            off += len + (len & 1);
-            rows++;
+            off += (len + 3) & ~3;
             if (is_dense) dense++; else max_sparse = std::max(max_sparse, ne);
+            if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
+        }
+        for (const auto &ch : chains) {
+            for (size_t j = 0; j < ch.size(); j++) ref[ch[j]] = (int32_t)(off + kChainEntry * j) | kRefChain;
+            off += kChainEntry * (int64_t)(ch.size() + 1);
+            chain_states += (int32_t)ch.size();
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
         }
         h->table.assign((size_t)off + kTablePad, 0);
         for (int32_t q = 0; q < G.nQ; q++) h->table[q] = ref[block[B.start_state[q]]];
         for (int32_t b : order) {
-            if (det[b] >= 0) continue;
+            if (det[b] >= 0 || is_thin(b)) continue;
             int32_t *row = h->table.data() + ref_offset(ref[b]);
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             row[0] = m_cls[b];
+            row[2] = ref[m_def[b]];
             row[3] = 0;
             if (ref_is_dense(ref[b])) {
                 row[1] = -1;
-                row[2] = ref[m_def[b]];
                 for (int32_t X = 0; X < G.nPi; X++) row[kRowHeader + X] = ref[m_def[b]];
                 for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) row[kRowHeader + m_sym[e]] = ref[m_tgt[e]];
             } else {
                 row[1] = ne;
-                row[2] = ref[m_def[b]];
                 for (int32_t e = 0; e < ne; e++) {
                     row[kRowHeader + 2 * e] = m_sym[m_ebeg[b] + e];
                     row[kRowHeader + 2 * e + 1] = ref[m_tgt[m_ebeg[b] + e]];
                 }
             }
         }
-        // Skip chains: a sparse row with no edges sends every symbol to its
-        // default, and default transitions accept nothing new, so the class
-        // is constant along a chain of such rows.  Its header then holds the
-        // chain length L (row[3]) and the state reached after L symbols
-        // (row[2]); a walk consumes the L symbols with one load.
-        int32_t max_chain = 0;
-        for (int32_t b : order) {
-            if (det[b] >= 0 || ref_is_dense(ref[b]) || m_ebeg[b + 1] != m_ebeg[b]) continue;
-            int32_t L = 0, cur = b;
-            while (true) {
-                bool skip = det[cur] < 0 && !ref_is_dense(ref[cur]) && m_ebeg[cur + 1] == m_ebeg[cur];
-                if (!skip || (L > 0 && m_cls[cur] != m_cls[b]) || L >= (1 << 20)) break;
-                L++;
-                cur = m_def[cur];
-                if (cur == b) throw BuildError(PSC_E_LIMIT, "cycle of edge-free rows");
+        for (const auto &ch : chains) {
+            int32_t *e = h->table.data() + ref_offset(ref[ch[0]]);
+            for (int32_t b : ch) {
+                const int32_t ce = cont_edge(b);
+                uint32_t a = ce < 0 ? (uint32_t)kSymWild : (uint32_t)m_sym[ce], bs = kSymNone;
+                int32_t rb = 0;
+                for (int32_t k = m_ebeg[b]; k < m_ebeg[b + 1]; k++)
+                    if (k != ce) { bs = (uint32_t)m_sym[k]; rb = ref[m_tgt[k]]; }
+                e[0] = (int32_t)(a | (bs << 16));
+                e[1] = rb;
+                e[2] = ref[m_def[b]];
+                e[3] = m_cls[b];
+                e += kChainEntry;
             }
-            int32_t *row = h->table.data() + ref_offset(ref[b]);
-            row[2] = ref[cur];
-            row[3] = L;
-            max_chain = std::max(max_chain, L);
+            e[0] = (int32_t)((uint32_t)kSymJump | ((uint32_t)kSymNone << 16));
+            e[1] = 0;
+            e[2] = ref[cont_target(ch.back())];
+            e[3] = 0;
         }
         h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);
         for (int32_t c = 0; c < h->n_classes; c++)
@@ -1150,6 +1182,8 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         I.dfa_rows = rows;
         I.dense_rows = dense;
         I.max_sparse_edges = max_sparse;
+        I.chain_states = chain_states;
+        I.chains = (int32_t)chains.size();
         I.table_bytes = (int64_t)h->table.size() * 4;
         I.mask_table_bytes = (int64_t)h->masks.size() * 4;
         I.device_bytes = (int64_t)h->device_bytes_needed();
@@ -1195,19 +1229,20 @@ extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stac
         for (;;) {
             if (ref_is_class(ref)) { cls = ref_class(ref); break; }
             const int32_t *row = T + ref_offset(ref);
-            if (i < 0) { cls = row[0]; break; }
-            if (!ref_is_dense(ref) && row[1] == 0) {      // skip chain of row[3] symbols
-                int32_t L = row[3], t = std::min(L, i + 1);
-                bool bad = false;
-                for (int32_t k = 0; k < t; k++) bad |= st[i - k] < 0 || st[i - k] >= h->n_lr;
-                if (bad) { cls = -1; break; }
-                i -= t;
-                if (t < L) { cls = row[0]; break; }
-                ref = row[2];
+            if (ref_is_chain(ref)) {                         // one chain entry at a time
+                const uint32_t x = (uint32_t)row[0];
+                const int32_t a = (int32_t)(x & 0xFFFF), bs = (int32_t)(x >> 16);
+                if (a == kSymJump) { ref = row[2]; continue; }
+                if (i < 0) { cls = row[3]; break; }
+                const int32_t X = st[i--];
+                if (X < 0 || X >= h->n_lr) break;
+                if (a == kSymWild || X == a) ref = (ref_offset(ref) + kChainEntry) | kRefChain;
+                else ref = X == bs ? row[1] : row[2];
                 continue;
             }
-            int32_t X = st[i--];
-            if (X < 0 || X >= h->n_lr) { cls = -1; break; }
+            if (i < 0) { cls = row[0]; break; }
+            const int32_t X = st[i--];
+            if (X < 0 || X >= h->n_lr) break;
             if (ref_is_dense(ref)) {
                 ref = row[kRowHeader + X];
             } else {

@@ -42,20 +42,25 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
 // Walk of sequence b by one wavefront (Algorithm 2, classification step):
 // ref = start[q]; read the stack top-first; stop as soon as ref names a
 // class (a determined state).  The walk is a chain of dependent loads, so
-// every step is exactly ONE wavefront-wide vector load of the current row:
-//   sparse row: lane 0 <- (end_class, n_edges), lane 1 <- (default, skip),
+// every step is exactly ONE wavefront-wide vector load from the table:
+//   sparse row: lane 0 <- (end_class, n_edges), lane 1 <- (default, -),
 //               lane j >= 2 <- edge j-2 as (symbol, ref); the edge matching
 //               the symbol is found with a ballot and read with readlane;
 //   dense row:  lane 0 <- (end_class, -), lane 1 <- entry[symbol];
-//   edge-free sparse row: a skip chain, L symbols consumed at once (only
-//               range checked).
+//   chain:      lane j <- the j-th entry from the current state; lane j
+//               compares it with the j-th next stack symbol (a cross-lane
+//               shuffle of the staged window), and a ballot finds the first
+//               entry the walk does not pass: up to kChunk symbols per load.
+// The stack is staged in a window of kChunk symbols in VGPRs (lane j holds
+// the j-th symbol below the window's top, stack index chunk_base - j).
 // Before the walk: round trip 1 fetches lens[b], qs[b] and the lengths before
-// b (start offset); round trip 2 fetches the top kChunk stack symbols (lane j
-// holds the j-th symbol below the chunk's top) together with start[q] in
-// lane 63.  Returns the class id, or -1 for a rejected input (length <= 0,
-// lexer state or stack symbol out of range); the result is wave-uniform.
+// b (start offset); round trip 2 fetches the top window together with
+// start[q] in lane 63.  Returns the class id, or -1 for a rejected input
+// (length <= 0, lexer state or stack symbol out of range); the result is
+// wave-uniform.
 constexpr int kChunk = kWave - 1;
 static_assert(kSparseMax <= kWave - 2, "a sparse row must fit one wavefront load");
+static_assert(kChainMax <= kChunk, "a chain must end within one wavefront load");
 
 __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                           const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
@@ -73,7 +78,7 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
         const int32_t *st = stacks + off;
         int i = len - 1;           // index of the next symbol to read
         int chunk_base = i;        // stack index held by lane 0
-        // round trip 2: stack chunk + start[q]
+        // round trip 2: stack window + start[q]
         const int32_t *a0 = lane == kChunk ? table + q
                           : (chunk_base - lane >= 0 ? st + (chunk_base - lane) : table + q);
         int sym = *a0;
@@ -84,49 +89,55 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
                 chunk_base = i;
                 sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
             }
+            const int32_t *row = table + (ref & ~3);
+            if ((ref & 3) == kRefChain) {
+                const int4 e = *reinterpret_cast<const int4 *>(row + kChainEntry * lane);
+                const int pos = chunk_base - i;          // window lane of stack index i
+                const int src = pos + lane;              // window lane of stack index i - lane
+                const int Xl = __shfl(sym, src & (kWave - 1), kWave);
+                const int a = e.x & 0xFFFF;
+                const bool pass = a != kSymJump && i - lane >= 0 && src < kChunk && Xl >= 0 && Xl < n_lr &&
+                                  (a == kSymWild || Xl == a);
+                // lane 63 never passes (src >= kChunk), so f <= 63
+                const int f = __ffsll((long long)__ballot(!pass)) - 1;
+                const int fx = __builtin_amdgcn_readlane(e.x, f);
+                if ((fx & 0xFFFF) == kSymJump) {          // end of the chain: go on without reading
+                    i -= f;
+                    ref = __builtin_amdgcn_readlane(e.z, f);
+                    continue;
+                }
+                if (i - f < 0) { cls = __builtin_amdgcn_readlane(e.w, f); break; }   // stack ended
+                if (pos + f >= kChunk) {                  // window used up: restage, resume at entry f
+                    i -= f;
+                    ref = ((ref & ~3) + kChainEntry * f) | kRefChain;
+                    continue;
+                }
+                const int fX = __builtin_amdgcn_readlane(Xl, f);
+                if (fX < 0 || fX >= n_lr) break;
+                i -= f + 1;
+                ref = fX == (int)((uint32_t)fx >> 16) ? __builtin_amdgcn_readlane(e.y, f)
+                                                      : __builtin_amdgcn_readlane(e.z, f);
+                continue;
+            }
             const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
             const bool x_ok = X >= 0 && X < n_lr;
-            const int32_t *row = table + (ref & ~1);
-            const bool dense = ref & 1;
-            // the one load of this step: one aligned 8-byte load per lane
-            // (a dense row's lane 1 takes the aligned pair holding entry X)
+            const bool dense = (ref & 3) == kRefDense;
+            // one aligned 8-byte load per lane (a dense row's lane 1 takes
+            // the aligned pair holding entry X)
             const int Xc = x_ok ? X : 0;
             const int ia = dense ? (lane == 0 ? 0 : kRowHeader + (Xc & ~1)) : 2 * lane;
             const int2 v = *reinterpret_cast<const int2 *>(row + ia);
             const int va = v.x, vc = v.y;
             if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); break; }
-            if (dense) {
-                if (!x_ok) break;
-                ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
-                i--;
-                continue;
-            }
-            const int n = __builtin_amdgcn_readlane(vc, 0);
-            if (n == 0) {                                    // skip chain
-                const int L = max(__builtin_amdgcn_readlane(vc, 1), 1);   // >= 1: always progresses
-                const int t = min(L, i + 1);
-                int left = t;
-                bool bad = false;
-                while (left > 0) {
-                    if (chunk_base - i >= kChunk) {
-                        chunk_base = i;
-                        sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
-                    }
-                    const int pos = chunk_base - i;
-                    const int take = min(left, kChunk - pos);
-                    bad |= __ballot(lane >= pos && lane < pos + take && (sym < 0 || sym >= n_lr)) != 0;
-                    i -= take;
-                    left -= take;
-                }
-                if (bad) break;
-                if (t < L) { cls = __builtin_amdgcn_readlane(va, 0); break; }
-                ref = __builtin_amdgcn_readlane(va, 1);
-                continue;
-            }
             if (!x_ok) break;
-            const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
-            ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
-                      : __builtin_amdgcn_readlane(va, 1);
+            if (dense) {
+                ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
+            } else {
+                const int n = __builtin_amdgcn_readlane(vc, 0);
+                const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
+                ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
+                          : __builtin_amdgcn_readlane(va, 1);
+            }
             i--;
         }
     }

@@ -11,28 +11,45 @@
 namespace psc {
 
 // A reference to an automaton state as stored in the flat table:
-//   ref >= 0 : the state's row starts at int32 offset (ref & ~1) of the
-//              table; bit 0 set means the row is dense over the stack
-//              alphabet, clear means sparse (sorted (symbol, ref) pairs).
+//   ref >= 0 : the state's row or chain entry starts at int32 offset
+//              (ref & ~3) of the table; the low two bits give its kind:
+//              0 sparse row, 1 dense row, 2 chain entry.
 //   ref <  0 : the state is determined -- every stack continuation ends in
 //              the same class -- and that class is (-ref - 1).
-// Row header (4 int32): end_class, n_edges (sparse) or -1 (dense),
-// default_ref (sparse), skip.  Sparse rows follow with n_edges pairs
-// (symbol, ref); dense rows with n_lr_states refs indexed by symbol.
-// A sparse row with n_edges == 0 heads a skip chain: every symbol leads to
-// the default and the class cannot change, so skip = L >= 1 symbols are
-// consumed at once and default_ref is the state reached after them (if the
-// stack ends inside the chain, the class is this row's end_class).
-// Rows start at even offsets so a pair is one aligned 8-byte load.
+// Sparse and dense rows have a 4-int32 header: end_class, n_edges (sparse)
+// or -1 (dense), default_ref, 0.  Sparse rows follow with n_edges pairs
+// (symbol, ref) sorted by symbol; dense rows with n_lr_states refs indexed
+// by symbol.
+//
+// Chains: a state with at most two explicit edges (an edge-free state
+// included) is one 16-byte entry of a chain, so that a walk through a run
+// of such "thin" states costs one load per up to kChainMax symbols instead
+// of one per symbol:
+//   x = a | (b << 16)  a: the symbol that moves on to the next entry of the
+//                      chain (kSymWild: any symbol), or kSymJump;
+//                      b: the other explicit edge's symbol, or kSymNone;
+//   y = ref on b;  z = ref on any other symbol (for kSymJump: the state the
+//   chain continues with, reached without reading a symbol);  w = the
+//   state's end_class (the class when the stack ends before it reads).
+// A chain holds at most kChainMax states and ends with a kSymJump entry, so
+// 64 consecutive entries read from any state of it include that entry.
+// Rows and entries start at multiples of 4 int32 (16-byte aligned).
 constexpr int kRowHeader = 4;
 constexpr int kSparseMax = 62;      // header + edges in one wavefront-wide load
-constexpr int kTablePad = 2 * 64 + kRowHeader;  // a row load reads 128 int32 speculatively
+constexpr int kChainMax = 63;
+constexpr int kChainEntry = 4;      // int32 per entry
+constexpr int32_t kSymNone = 0xFFFF, kSymWild = 0xFFFE, kSymJump = 0xFFFD;
+constexpr int kMaxChainAlphabet = 0xFFFD;   // chains need every symbol < kSymJump
+constexpr int kRefDense = 1, kRefChain = 2;
+// a walk step reads 64 lanes x 16 bytes from a chain entry speculatively
+constexpr int kTablePad = 64 * kChainEntry + kRowHeader;
 
 inline bool ref_is_class(int32_t ref) { return ref < 0; }
 inline int32_t ref_class(int32_t ref) { return -ref - 1; }
 inline int32_t class_ref(int32_t cls) { return -cls - 1; }
-inline bool ref_is_dense(int32_t ref) { return (ref & 1) != 0; }
-inline int32_t ref_offset(int32_t ref) { return ref & ~1; }
+inline bool ref_is_dense(int32_t ref) { return (ref & 3) == kRefDense; }
+inline bool ref_is_chain(int32_t ref) { return (ref & 3) == kRefChain; }
+inline int32_t ref_offset(int32_t ref) { return ref & ~3; }
 
 // Device buffer layout (offsets in bytes from the bound base):
 //   [0, 256)                   uint32 error counter (+ padding)

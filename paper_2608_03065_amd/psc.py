@@ -51,6 +51,7 @@ class Info(C.Structure):
         ("dfa_states_built", C.c_int64), ("dfa_states", C.c_int32), ("dfa_rows", C.c_int32),
         ("dense_rows", C.c_int32), ("max_sparse_edges", C.c_int32), ("table_bytes", C.c_int64),
         ("mask_table_bytes", C.c_int64), ("device_bytes", C.c_int64), ("build_seconds", C.c_double),
+        ("chain_states", C.c_int32), ("chains", C.c_int32),
     ]
 
     def as_dict(self) -> dict:
