@@ -53,107 +53,141 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
 //               entry the walk does not pass: up to kChunk symbols per load.
 // The stack is staged in a window of kChunk symbols in VGPRs (lane j holds
 // the j-th symbol below the window's top, stack index chunk_base - j).
-// Before the walk: round trip 1 fetches lens[b], qs[b] and the lengths before
-// b (start offset); round trip 2 fetches the top window together with
-// start[q] in lane 63.  Returns the class id, or -1 for a rejected input
-// (length <= 0, lexer state or stack symbol out of range); the result is
-// wave-uniform.
+// `st` is the stack (len >= 1 symbols, bottom first) and q its lexer state
+// (in range).  When the window is restaged, the next row load is issued
+// before the window is waited for.  Returns the class id, or -1 for a stack
+// symbol out of range; the result is wave-uniform.
 constexpr int kChunk = kWave - 1;
 static_assert(kSparseMax <= kWave - 2, "a sparse row must fit one wavefront load");
 static_assert(kChainMax <= kChunk, "a chain must end within one wavefront load");
 
-__device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
-                                          const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
-                                          const int32_t *__restrict__ qs, int b, int lane) {
-    // round trip 1 (all independent; vector loads so no scalar load queues
-    // behind the reduction)
-    const int own = *((lane & 1) ? qs + b : lens + b);
-    int part = lane < b ? lens[lane] : 0;
-    for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
-    const int len = __builtin_amdgcn_readlane(own, 0);
-    const int q = __builtin_amdgcn_readlane(own, 1);
-    const int off = wave_sum(part);
-    int cls = -1;   // -1 = rejected input
-    if (len > 0 && q >= 0 && q < n_lex) {
-        const int32_t *st = stacks + off;
-        int i = len - 1;           // index of the next symbol to read
-        int chunk_base = i;        // stack index held by lane 0
-        // round trip 2: stack window + start[q]
-        const int32_t *a0 = lane == kChunk ? table + q
-                          : (chunk_base - lane >= 0 ? st + (chunk_base - lane) : table + q);
-        int sym = *a0;
-        int ref = __builtin_amdgcn_readlane(sym, kChunk);
-        for (;;) {
-            if (ref < 0) { cls = -ref - 1; break; }
-            if (i >= 0 && chunk_base - i >= kChunk) {
-                chunk_base = i;
-                sym = (lane < kChunk && chunk_base - lane >= 0) ? st[chunk_base - lane] : 0;
-            }
-            const int32_t *row = table + (ref & ~3);
-            if ((ref & 3) == kRefChain) {
-                const int4 e = *reinterpret_cast<const int4 *>(row + kChainEntry * lane);
-                const int pos = chunk_base - i;          // window lane of stack index i
-                const int src = pos + lane;              // window lane of stack index i - lane
-                const int Xl = __shfl(sym, src & (kWave - 1), kWave);
-                const int a = e.x & 0xFFFF;
-                const bool pass = a != kSymJump && i - lane >= 0 && src < kChunk && Xl >= 0 && Xl < n_lr &&
-                                  (a == kSymWild || Xl == a);
-                // lane 63 never passes (src >= kChunk), so f <= 63
-                const int f = __ffsll((long long)__ballot(!pass)) - 1;
-                const int fx = __builtin_amdgcn_readlane(e.x, f);
-                if ((fx & 0xFFFF) == kSymJump) {          // end of the chain: go on without reading
-                    i -= f;
-                    ref = __builtin_amdgcn_readlane(e.z, f);
-                    continue;
-                }
-                if (i - f < 0) { cls = __builtin_amdgcn_readlane(e.w, f); break; }   // stack ended
-                if (pos + f >= kChunk) {                  // window used up: restage, resume at entry f
-                    i -= f;
-                    ref = ((ref & ~3) + kChainEntry * f) | kRefChain;
-                    continue;
-                }
-                const int fX = __builtin_amdgcn_readlane(Xl, f);
-                if (fX < 0 || fX >= n_lr) break;
-                i -= f + 1;
-                ref = fX == (int)((uint32_t)fx >> 16) ? __builtin_amdgcn_readlane(e.y, f)
-                                                      : __builtin_amdgcn_readlane(e.z, f);
-                continue;
-            }
-            const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
-            const bool x_ok = X >= 0 && X < n_lr;
-            const bool dense = (ref & 3) == kRefDense;
-            // one aligned 8-byte load per lane (a dense row's lane 1 takes
-            // the aligned pair holding entry X)
-            const int Xc = x_ok ? X : 0;
-            const int ia = dense ? (lane == 0 ? 0 : kRowHeader + (Xc & ~1)) : 2 * lane;
-            const int2 v = *reinterpret_cast<const int2 *>(row + ia);
-            const int va = v.x, vc = v.y;
-            if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); break; }
-            if (!x_ok) break;
-            if (dense) {
-                ref = (Xc & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
-            } else {
-                const int n = __builtin_amdgcn_readlane(vc, 0);
-                const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
-                ref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
-                          : __builtin_amdgcn_readlane(va, 1);
-            }
-            i--;
+constexpr int32_t kRefFault = INT32_MIN;   // no class ref is this small
+
+struct Walk {
+    const int32_t *__restrict__ table;
+    const int32_t *__restrict__ st;
+    int32_t n_lr;
+    int lane;
+    int i;            // index of the next stack symbol to read (wave-uniform)
+    int chunk_base;   // stack index held by window lane 0 (wave-uniform)
+    int sym;          // the window (lanes past the bottom hold st[0], never used)
+    int ref;          // current state (wave-uniform)
+    int cls;          // the result once the walk has ended
+
+    __device__ __forceinline__ void stage() { sym = st[max(chunk_base - lane, 0)]; }
+
+    // One step from a chain entry: lane j holds the j-th entry from the
+    // current state.  Returns true when the walk has ended.
+    __device__ __forceinline__ bool chain_step(const int4 e) {
+        const int pos = chunk_base - i;          // window lane of stack index i
+        const int src = pos + lane;              // window lane of stack index i - lane
+        const int Xl = __shfl(sym, src & (kWave - 1), kWave);
+        const int a = e.x & 0xFFFF;
+        const bool pass = a != kSymJump && i - lane >= 0 && src < kChunk && Xl >= 0 && Xl < n_lr &&
+                          (a == kSymWild || Xl == a);
+        // lane 63 never passes (src >= kChunk), so f <= 63
+        const int f = __ffsll((long long)__ballot(!pass)) - 1;
+        const int fx = __builtin_amdgcn_readlane(e.x, f);
+        if ((fx & 0xFFFF) == kSymJump) {          // end of the chain: go on without reading
+            i -= f;
+            ref = __builtin_amdgcn_readlane(e.z, f);
+            return false;
         }
+        if (i - f < 0) { cls = __builtin_amdgcn_readlane(e.w, f); return true; }   // stack ended
+        if (pos + f >= kChunk) {                  // window used up: restage, resume at entry f
+            i -= f;
+            ref = ((ref & ~3) + kChainEntry * f) | kRefChain;
+            return false;
+        }
+        const int fX = __builtin_amdgcn_readlane(Xl, f);
+        if (fX < 0 || fX >= n_lr) { cls = -1; return true; }
+        i -= f + 1;
+        ref = fX == (int)((uint32_t)fx >> 16) ? __builtin_amdgcn_readlane(e.y, f)
+                                              : __builtin_amdgcn_readlane(e.z, f);
+        return false;
     }
-    return cls;
+
+    // One step from a sparse row (lane 0: end_class, n_edges; lane 1:
+    // default; lane j >= 2: edge j-2) or a dense row (lane 0: end_class;
+    // lane 1: the aligned pair holding entry X).
+    __device__ __forceinline__ bool row_step(const int2 v, bool dense, int X) {
+        const int va = v.x, vc = v.y;
+        if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); return true; }
+        int nref;
+        if (dense) {
+            nref = (X & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
+        } else {
+            const int n = __builtin_amdgcn_readlane(vc, 0);
+            const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
+            nref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
+                       : __builtin_amdgcn_readlane(va, 1);
+        }
+        // a symbol out of range ends the walk through kRefFault; a select,
+        // not a branch, so that the row load cannot sink below the window
+        ref = X >= 0 && X < n_lr ? nref : kRefFault;
+        i--;
+        return false;
+    }
+
+    // One step: the one table load, then its evaluation.  A chain or sparse
+    // row is loaded before the window is read.
+    __device__ __forceinline__ bool step() {
+        const int32_t *row = table + (ref & ~3);
+        if ((ref & 3) == kRefChain) return chain_step(*reinterpret_cast<const int4 *>(row + kChainEntry * lane));
+        if ((ref & 3) == kRefDense) {
+            const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+            const int Xd = X >= 0 && X < n_lr ? X : 0;
+            const int2 v = *reinterpret_cast<const int2 *>(row + (lane == 0 ? 0 : kRowHeader + (Xd & ~1)));
+            return row_step(v, true, X);
+        }
+        const int2 v = *reinterpret_cast<const int2 *>(row + 2 * lane);
+        const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+        return row_step(v, false, X);
+    }
+};
+
+__device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lr,
+                                          const int32_t *__restrict__ st, int len, int q, int lane) {
+    Walk w{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1};
+    // round trip 2: the window, with start[q] in lane 63
+    w.sym = lane == kChunk ? table[q] : st[max(w.chunk_base - lane, 0)];
+    w.ref = __builtin_amdgcn_readlane(w.sym, kChunk);
+    if (w.ref < 0) return -w.ref - 1;
+    if (w.step()) return w.cls;
+    for (;;) {
+        // ref, i and chunk_base are wave-uniform; saying so keeps the
+        // loop's branches scalar
+        w.ref = __builtin_amdgcn_readfirstlane(w.ref);
+        w.i = __builtin_amdgcn_readfirstlane(w.i);
+        w.chunk_base = __builtin_amdgcn_readfirstlane(w.chunk_base);
+        if (w.ref < 0) return w.ref == kRefFault ? -1 : -w.ref - 1;
+        if (w.i >= 0 && w.chunk_base - w.i >= kChunk) {
+            w.chunk_base = w.i;
+            w.stage();
+        }
+        if (w.step()) return w.cls;
+    }
 }
 
 // Wavefront 0 of the workgroup walks sequence b; the class (or -1) is
 // published to the whole workgroup through LDS.  Slice 0 of each sequence
-// counts rejected inputs.
+// counts rejected inputs.  Round trip 1 fetches lens[b], qs[b] and the
+// lengths before b (the stack's offset).
 __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                            const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
                                            const int32_t *__restrict__ qs, int b, uint32_t *__restrict__ err) {
     __shared__ int32_t s_cls;
     if (threadIdx.x < kWave) {
-        const int cls = walk_class(table, n_lex, n_lr, stacks, lens, qs, b, threadIdx.x);
-        if (threadIdx.x == 0) {
+        const int lane = threadIdx.x;
+        const int own = *((lane & 1) ? qs + b : lens + b);
+        int part = lane < b ? lens[lane] : 0;
+        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+        const int len = __builtin_amdgcn_readlane(own, 0);
+        const int q = __builtin_amdgcn_readlane(own, 1);
+        const int off = wave_sum(part);
+        int cls = -1;
+        if (len > 0 && q >= 0 && q < n_lex) cls = walk_class(table, n_lr, stacks + off, len, q, lane);
+        if (lane == 0) {
             s_cls = cls;
             if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
         }
