@@ -255,8 +255,9 @@ def main():
                            "one_pass_read_write_model": round(one_pass_model)},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "build": {k: info[k] for k in ("dfa_states", "n_classes", "table_bytes", "mask_table_bytes",
-                                        "build_seconds", "dfa_rows", "dense_rows")},
+        "build": {k: info[k] for k in ("dfa_states_built", "dfa_states", "n_classes", "table_bytes",
+                                        "mask_table_bytes", "build_seconds", "dfa_rows", "dense_rows",
+                                        "chain_states", "chains")},
     }
     print(json.dumps(out), flush=True)
 
