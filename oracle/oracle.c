@@ -31,6 +31,11 @@
  *
  * Masks are packed LSB-first into uint32 words, W = ceil(V/32), tail bits 0.
  *
+ * It also advances a prefix state by one token (oracle_advance): the new
+ * state after x.v is what lexing v from q and feeding the terminals it emits
+ * leaves behind, with the last lexeme still pending in the lexer state
+ * (Sec. 3.2: the prefix state is the lexer state plus the parser stack).
+ *
  * Build: gcc -O2 -fopenmp -shared -fPIC -o liboracle.so oracle.c
  */
 #include <stdint.h>
@@ -277,4 +282,59 @@ void oracle_token_bits(const void *ctx, const int32_t *alpha, int32_t len, int32
     for (int64_t i = 0; i < n; i++) out[i] = (uint8_t)token_allowed(o, q, alpha, len, toks[i], v, sc);
     free(v);
     free(sc);
+}
+
+/* The prefix state after one more token (Sec. 3.2; Alg. 2's lexing and
+ * parsing steps, which produce the next (q, alpha)).  Lex tok's bytes from q
+ * and feed every emitted terminal; the lexeme pending after the last byte
+ * stays in the lexer state and is not fed.  EOS feeds the pending lexeme's
+ * terminal (if any) and then $end.  Returns
+ *   0  advanced: (*q_out, out[0 .. *len_out)) is the new state;
+ *   1  rejected: the lexer has no move, or an emitted terminal is not shifted
+ *      (this does not look ahead: a token can be advanced over and still leave
+ *      a pending lexeme that nothing completes -- the mask rejects those);
+ *   2  EOS accepted: x is a sentence of the language (state unchanged);
+ *   3  the new stack would be longer than cap. */
+int oracle_advance(const void *ctx, int32_t q, const int32_t *alpha, int32_t len, int32_t tok, int32_t cap,
+                   int32_t *q_out, int32_t *out, int32_t *len_out) {
+    const oracle_ctx *o = (const oracle_ctx *)ctx;
+    const or_grammar *g = &o->g;
+    view *v = (view *)malloc(sizeof(view));
+    v->alpha = alpha;
+    v->depth = len;
+    v->n = 0;
+    int32_t cur = q;
+    int status = 0;
+    if (tok == o->eos) {
+        status = 2;
+        if (cur != 0) {
+            int32_t t = g->lex_accept[cur];
+            if (t < 0 || (!g->ignored[t] && !feed(g, v, t))) status = 1;
+        }
+        if (status == 2 && !feed(g, v, g->end_term)) status = 1;
+        free(v);
+        return status;
+    }
+    for (int64_t i = o->voffs[tok]; i < o->voffs[tok + 1] && status == 0; i++) {
+        uint8_t c = o->vbytes[i];
+        int32_t nx = g->lex_next[(int64_t)cur * 256 + c];
+        if (nx >= 0) { cur = nx; continue; }
+        if (cur == 0 || g->lex_accept[cur] < 0) { status = 1; break; }
+        int32_t t = g->lex_accept[cur];
+        if (!g->ignored[t] && !feed(g, v, t)) { status = 1; break; }
+        cur = g->lex_next[c];
+        if (cur < 0) status = 1;
+    }
+    if (status == 0) {
+        if (v->depth + v->n > cap) {
+            status = 3;
+        } else {
+            memcpy(out, alpha, (size_t)v->depth * sizeof(int32_t));
+            memcpy(out + v->depth, v->s, (size_t)v->n * sizeof(int32_t));
+            *len_out = v->depth + v->n;
+            *q_out = cur;
+        }
+    }
+    free(v);
+    return status;
 }

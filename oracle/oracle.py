@@ -35,6 +35,8 @@ def _load():
         lib.oracle_masks.argtypes = [P, P, P, P, P, C.c_int32, P, C.c_int32]
         lib.oracle_masks.restype = C.c_int
         lib.oracle_token_bits.argtypes = [P, P, C.c_int32, C.c_int32, P, C.c_int64, P]
+        lib.oracle_advance.argtypes = [P, C.c_int32, P, C.c_int32, C.c_int32, C.c_int32, P, P, P]
+        lib.oracle_advance.restype = C.c_int
         _lib = lib
     return _lib
 
@@ -118,6 +120,25 @@ class Oracle:
         _load().oracle_token_bits(self._ctx, stack.ctypes.data, n, int(q), toks.ctypes.data,
                                   len(toks), out.ctypes.data)
         return out.astype(bool)
+
+    ADVANCED, REJECTED, EOS_ACCEPTED, OVERFLOW = 0, 1, 2, 3
+
+    def advance(self, state, tok: int, cap: int | None = None):
+        """One token on a prefix state: (status, new state or None).  Status
+        0 advanced, 1 rejected, 2 EOS accepted (state unchanged), 3 the new
+        stack would be longer than cap (default: no practical limit)."""
+        q, stack = state
+        stack = np.ascontiguousarray(stack, dtype=np.int32)
+        n = stack.size
+        if cap is None:
+            cap = n + 8192
+        buf = np.zeros(max(cap, 1), np.int32)
+        qo, lo = C.c_int32(0), C.c_int32(0)
+        st = _load().oracle_advance(self._ctx, int(q), (stack if n else np.zeros(1, np.int32)).ctypes.data, n,
+                                    int(tok), int(cap), C.byref(qo), buf.ctypes.data, C.byref(lo))
+        if st != 0:
+            return st, None
+        return 0, (int(qo.value), buf[:lo.value].copy())
 
 
 def unpack(mask_row: np.ndarray, V: int) -> np.ndarray:
