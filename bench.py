@@ -43,6 +43,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--warm-cache", action="store_true", help="single logits buffer (cache-resident; labelled)")
+    ap.add_argument("--decode-steps", type=int, default=256,
+                    help="tokens per sequence in the on-device decoding loop (advance + masks)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
@@ -161,6 +163,11 @@ def main():
         t_apply = loop(only_apply, 1000)     # masks of steps 0..n_bm-1, as counted below
         t_compute = loop(only_compute, 1000)
 
+        # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
+        # advanced by one token each (psc_advance), then the single-launch
+        # step on them (psc_compute_and_apply_dense)
+        decode = decode_steps(wl, clf, B, pool, bms, stream, dev, args.decode_steps)
+
     # Algorithmic bytes, from the actual masks.  The apply touches logits per
     # 16-byte vector: one whose entries are all masked is written once
     # (16 B); one that keeps some entries and masks others must be read to be
@@ -248,6 +255,7 @@ def main():
         },
         "step_mode": args.mode,
         "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
+        "decode_step_us": decode,
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
                        "apply_mask_solo_gbs": round(achieved_apply, 1)},
         "bytes_per_step": {"algorithmic": round(bytes_step), "fused": round(bytes_fused),
@@ -260,6 +268,63 @@ def main():
                                         "chain_states", "chains")},
     }
     print(json.dumps(out), flush=True)
+
+
+def decode_steps(wl, clf, B, pool, bms, stream, dev, max_steps):
+    """Per-token time of the grammar side of decoding with the prefix states
+    kept on the GPU: psc_advance (one token per sequence), alone and followed
+    by psc_compute_and_apply_dense.  Each sequence follows a document of the
+    workload, tokenised by longest match; the final states are checked against
+    the input generator's host parser."""
+    import numpy as np
+    import torch
+
+    from inputs.seeds import rng_for
+    from paper_2608_03065_amd.psc import DecodeStates
+    toks, texts = [], []
+    for b in range(B):
+        best = b""
+        for k in range(8):                      # a document of at least max_steps tokens if one comes
+            d = wl.make_document(rng_for(wl.index, 0xDEC, b, k), wl)
+            if len(d) > len(best):
+                best = d
+            if len(wl.vocab.tokenize(best)) >= max_steps:
+                break
+        texts.append(best)
+        toks.append(wl.vocab.tokenize(best))
+    n = max(1, min(max_steps, min(len(t) for t in toks)))
+    cap = 4096
+    tok_dev = torch.tensor(np.array([t[:n] for t in toks], np.int32).T.copy(), device=dev)   # [n, B]
+    ds = DecodeStates(clf, B, cap, dev, stream)
+    n_pool, n_bm = len(pool), len(bms)
+
+    def run(with_masks):
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ds.reset(stream)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for k in range(n):
+            ds.advance(tok_dev[k], stream)
+            if with_masks:
+                ds.compute_and_apply(pool[k % n_pool], out=bms[k % n_bm], stream=stream)
+        z.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / n * 1e3
+
+    run(True)
+    t_both = run(True)
+    t_adv = run(False)
+    # the states after n tokens equal the host parser's at the same cut
+    got = ds.host_states()
+    ok = True
+    for b in range(B):
+        cut = sum(len(wl.vocab.tokens[t]) for t in toks[b][:n])
+        q, st = wl.host.states_at(texts[b], [cut])[0]
+        ok &= got[b][0] == q and np.array_equal(got[b][1], st)
+    if not ok:
+        raise RuntimeError("device states after the decoding loop differ from the host parser's")
+    return {"advance_and_fused_step": round(t_both, 3), "advance": round(t_adv, 3), "tokens_per_sequence": n,
+            "cap": cap, "states_checked": True}
 
 
 def measured_traffic(workload: str, kernel: str):

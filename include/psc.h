@@ -61,7 +61,8 @@ typedef enum { PSC_F32 = 0, PSC_BF16 = 1 } psc_dtype;
  *  goto_table [n_lr_states][n_nonterminals]  -1 = none.
  *  prod_lhs, prod_len [n_productions]        production 0 is the augmented
  *                                  start production.
- * Parser stacks are sequences of LR state ids (the stack alphabet Pi).
+ * Parser stacks are sequences of LR state ids (the stack alphabet Pi); LR
+ * state 0 is the parser's start state, so the empty prefix has stack [0].
  */
 typedef struct {
     int32_t n_lex_states;
@@ -132,9 +133,10 @@ psc_status psc_info(const psc_handle *h, psc_info_t *out);
 size_t psc_device_bytes(const psc_handle *h);
 
 /*
- * Copy the classifier and mask tables into caller-allocated device memory
- * (dev_buf, nbytes >= psc_device_bytes, 256-byte aligned) on `stream`, and
- * zero the device error counter.  The buffer must stay alive and unmodified
+ * Copy the classifier and mask tables, and the lexer, parser and vocabulary
+ * that psc_advance reads, into caller-allocated device memory (dev_buf,
+ * nbytes >= psc_device_bytes, 256-byte aligned) on `stream`, and zero the
+ * device error counter.  The buffer must stay alive and unmodified
  * while the handle is used; the handle keeps only the pointer.  Rebinding
  * replaces the previous binding.  Errors: PSC_E_INVALID_ARG, PSC_E_DEVICE.
  */
@@ -190,6 +192,66 @@ psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask
 psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                  const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
                                  psc_dtype dtype, int32_t V, void *stream);
+
+/*
+ * Device-resident prefix states (Sec. 3.2: a prefix is represented by its
+ * lexer state and parser stack; Algorithm 2 lexes and parses each new token
+ * before classifying).  B sequences keep their states in HBM between decoding
+ * steps, in a dense layout:
+ *  stacks        device int32 [B][cap]; stack b is stacks[b*cap .. b*cap +
+ *                stack_lens[b]), bottom first (LR state 0, the parser's start
+ *                state, at the bottom), top last.
+ *  stack_lens    device int32 [B], 1 <= stack_lens[b] <= cap.
+ *  lexer_states  device int32 [B].
+ * All three are caller-owned and updated in place by psc_state_reset and
+ * psc_advance; the masks of the states are computed by the *_dense calls.
+ */
+
+/* Status per sequence written by psc_advance. */
+enum {
+    PSC_ADV_OK = 0,        /* advanced: the new state is in place                          */
+    PSC_ADV_REJECTED = 1,  /* the lexer has no move or an emitted terminal is not shifted;
+                              state unchanged                                             */
+    PSC_ADV_EOS = 2,       /* EOS and the prefix is a sentence of the language; unchanged  */
+    PSC_ADV_OVERFLOW = 3,  /* the new stack would not fit cap, or the token pushes more
+                              than 192 states above what it keeps; unchanged              */
+    PSC_ADV_BAD_INPUT = 4, /* token, length, lexer state or a stack symbol the token's
+                              parsing reads out of range; unchanged                       */
+    PSC_ADV_SKIPPED = 5    /* tokens[b] < 0: nothing to do                                 */
+};
+
+/* Every sequence to the empty prefix: lexer state 0 (q0), stack [0].
+ * Errors: PSC_E_INVALID_ARG, PSC_E_DEVICE. */
+psc_status psc_state_reset(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,
+                           int32_t *lexer_states, int32_t B, void *stream);
+
+/*
+ * Advance every sequence b by token tokens[b] (device int32 [B]; < 0 = skip),
+ * the lexing and parsing steps of Algorithm 2 (Sec. 3.2): the token's bytes
+ * are lexed from the lexer state (longest match, one byte of lookahead), every
+ * terminal a finished lexeme yields is fed to the LR parser (its reductions,
+ * then a shift), and the lexeme still pending after the last byte stays in
+ * the lexer state.  EOS instead checks that the prefix is a sentence.  Writes
+ * status[b] (device int32 [B], PSC_ADV_*); the state changes only with
+ * PSC_ADV_OK.  It does not look ahead: a token can be advanced over and leave
+ * a pending lexeme that nothing can complete -- the next mask is then all
+ * zero (the masks reject such tokens beforehand).  Errors: PSC_E_INVALID_ARG,
+ * PSC_E_NOT_BOUND, PSC_E_DEVICE.
+ */
+psc_status psc_advance(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,
+                       int32_t *lexer_states, int32_t B, const int32_t *tokens, int32_t *status, void *stream);
+
+/* psc_compute_masks on device-resident states (dense layout above); a
+ * length outside [1, cap] is a rejected input. */
+psc_status psc_compute_masks_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                   const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                   uint32_t *out_bitmask, void *stream);
+
+/* psc_compute_and_apply on device-resident states (dense layout above). */
+psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                       const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                       uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                       void *stream);
 
 /* Read (synchronously, on `stream`) and optionally reset the device counter
  * of sequences that psc_compute_masks rejected as out of range. */

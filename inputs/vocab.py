@@ -31,6 +31,27 @@ class Vocab:
             blob = np.zeros(1, np.uint8)
         return blob, offs
 
+    def tokenize(self, text: bytes) -> list[int]:
+        """Longest-match tokenisation of text over the spellings (teacher
+        forcing); raises ValueError if the text cannot be covered."""
+        index = self.__dict__.get("_index")
+        if index is None:
+            index = {t: i for i, t in enumerate(self.tokens) if i != self.eos_id and t}
+            self.__dict__["_index"] = index
+            self.__dict__["_maxlen"] = max(len(t) for t in index)
+        maxlen = self.__dict__["_maxlen"]
+        out, i = [], 0
+        while i < len(text):
+            for L in range(min(maxlen, len(text) - i), 0, -1):
+                j = index.get(text[i:i + L])
+                if j is not None:
+                    out.append(j)
+                    i += L
+                    break
+            else:
+                raise ValueError("text not coverable by the vocabulary")
+        return out
+
     def length_histogram(self) -> dict[int, int]:
         h: dict[int, int] = {}
         for t in self.tokens:

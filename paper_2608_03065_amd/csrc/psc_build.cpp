@@ -905,9 +905,41 @@ std::vector<int32_t> minimise(const Automaton &B, int32_t *n_blocks_out) {
 using namespace psc;
 
 size_t psc_handle::device_bytes_needed() const {
-    size_t tb = (table.size() * sizeof(int32_t) + 255) & ~(size_t)255;
-    return kTableOff + tb + masks.size() * sizeof(uint32_t);
+    auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
+    return kTableOff + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
+           up(gram.size() * sizeof(int32_t)) + vbytes.size();
 }
+
+namespace {
+// Keep the problem instance for the device advance (the lexing and parsing
+// steps of Algorithm 2 run on the GPU between classifications).
+void copy_advance_tables(psc_handle *h, const psc_grammar *g, const psc_vocab *v) {
+    AdvanceLayout &L = h->adv;
+    std::vector<int32_t> &B = h->gram;
+    auto put = [&](int64_t &at, const int32_t *src, int64_t n) {
+        at = (int64_t)B.size();
+        B.insert(B.end(), src, src + n);
+    };
+    put(L.lex_next, g->lex_next, (int64_t)g->n_lex_states * 256);
+    put(L.lex_accept, g->lex_accept, g->n_lex_states);
+    L.ignored = (int64_t)B.size();
+    for (int32_t t = 0; t < g->n_terminals; t++) B.push_back(g->terminal_ignored[t] ? 1 : 0);
+    put(L.action, g->action, (int64_t)g->n_lr_states * g->n_terminals);
+    put(L.go, g->goto_table, (int64_t)g->n_lr_states * g->n_nonterminals);
+    put(L.prod_lhs, g->prod_lhs, g->n_productions);
+    put(L.prod_len, g->prod_len, g->n_productions);
+    const int64_t total = v->offsets[v->n_tokens];
+    if (total >= INT32_MAX) throw BuildError(PSC_E_LIMIT, "vocabulary spellings exceed 2 GiB");
+    L.tok_off = (int64_t)B.size();
+    for (int32_t t = 0; t <= v->n_tokens; t++) B.push_back((int32_t)v->offsets[t]);
+    L.n_term = g->n_terminals;
+    L.n_nt = g->n_nonterminals;
+    L.end_term = g->end_terminal;
+    L.eos = v->eos_id;
+    h->vbytes.assign(v->bytes ? v->bytes : nullptr, v->bytes ? v->bytes + total : nullptr);
+    if (h->vbytes.empty()) h->vbytes.push_back(0);
+}
+}  // namespace
 
 extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out) {
     auto t0 = std::chrono::steady_clock::now();
@@ -1069,13 +1101,15 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         }
 
         // flatten
-        psc_handle *h = new psc_handle();
+        std::unique_ptr<psc_handle> owned(new psc_handle());
+        psc_handle *h = owned.get();
         h->V = vocab->n_tokens;
         h->W = (vocab->n_tokens + 31) / 32;
         h->mask_stride = (h->W + 63) & ~63;   // 256-byte rows
         h->n_lex = G.nQ;
         h->n_lr = G.nPi;
         h->n_classes = (int32_t)kept.size();
+        copy_advance_tables(h, grammar, vocab);
         std::vector<int32_t> ref(nb, 0);
         // Thin states (at most two explicit edges) become chain entries.  A
         // thin state moves on along its lowest explicit edge into a thin
@@ -1188,7 +1222,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         I.mask_table_bytes = (int64_t)h->masks.size() * 4;
         I.device_bytes = (int64_t)h->device_bytes_needed();
         I.build_seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-        *out = h;
+        *out = owned.release();
         return PSC_OK;
     } catch (const BuildError &e) {
         set_error(std::string("psc_build: ") + e.what());

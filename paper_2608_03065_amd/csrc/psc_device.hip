@@ -171,22 +171,28 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
 
 // Wavefront 0 of the workgroup walks sequence b; the class (or -1) is
 // published to the whole workgroup through LDS.  Slice 0 of each sequence
-// counts rejected inputs.  Round trip 1 fetches lens[b], qs[b] and the
-// lengths before b (the stack's offset).
+// counts rejected inputs.  Round trip 1 fetches lens[b], qs[b] and, for
+// ragged stacks (stride 0), the lengths before b (the stack's offset); with
+// stride > 0 stack b starts at b * stride and holds at most stride symbols.
 __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
-                                           const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
-                                           const int32_t *__restrict__ qs, int b, uint32_t *__restrict__ err) {
+                                           const int32_t *__restrict__ stacks, int32_t stride,
+                                           const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
+                                           int b, uint32_t *__restrict__ err) {
     __shared__ int32_t s_cls;
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
         const int own = *((lane & 1) ? qs + b : lens + b);
-        int part = lane < b ? lens[lane] : 0;
-        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+        int part = 0;
+        if (stride == 0) {
+            part = lane < b ? lens[lane] : 0;
+            for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+        }
         const int len = __builtin_amdgcn_readlane(own, 0);
         const int q = __builtin_amdgcn_readlane(own, 1);
-        const int off = wave_sum(part);
+        const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
         int cls = -1;
-        if (len > 0 && q >= 0 && q < n_lex) cls = walk_class(table, n_lr, stacks + off, len, q, lane);
+        if (len > 0 && (stride == 0 || len <= stride) && q >= 0 && q < n_lex)
+            cls = walk_class(table, n_lr, stacks + off, len, q, lane);
         if (lane == 0) {
             s_cls = cls;
             if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
@@ -203,12 +209,12 @@ __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, in
 __global__ void __launch_bounds__(kBlock)
 walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks,
                    int32_t mask_stride, int32_t n_lex, int32_t n_lr,
-                   const int32_t *__restrict__ stacks, const int32_t *__restrict__ lens,
+                   const int32_t *__restrict__ stacks, int32_t stride, const int32_t *__restrict__ lens,
                    const int32_t *__restrict__ qs, int32_t B, int32_t W,
                    uint32_t *__restrict__ out, uint32_t *__restrict__ err, int32_t vec4) {
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
-    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int w0 = blockIdx.x * kCopyWordsPerBlock;
     const int w1 = min(W, w0 + kCopyWordsPerBlock);
     uint32_t *dst = out + (size_t)b * W;
@@ -332,12 +338,12 @@ apply_generic_kernel(void *__restrict__ logits, const uint32_t *__restrict__ bit
 template <bool kBf16>
 __global__ void __launch_bounds__(kBlock)
 fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
                   const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
                   uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
     using G = ApplyGeom<kBf16>;
     const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1);
     const int w_base = (blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * G::kWordsPerWave;
     if (w_base >= W) return;
@@ -359,12 +365,12 @@ static_assert(kGenWords <= kBlock, "one pass stages the slice's words");
 template <bool kBf16>
 __global__ void __launch_bounds__(kBlock)
 fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
                      const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
                      uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
     __shared__ uint32_t s_m[kGenWords];
     const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, lens, qs, b, err);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int w0 = blockIdx.x * kGenWords;
     const int nw = min(kGenWords, W - w0);
     if (threadIdx.x < nw) {
@@ -382,9 +388,240 @@ fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restri
     }
 }
 
+// ---------------------------------------------------------------- advance
+
+// The problem instance on the device (the lexing and parsing steps of
+// Algorithm 2, which turn a prefix state and a token into the next state).
+struct AdvTables {
+    const int32_t *lex_next, *lex_accept, *ignored, *action, *go, *prod_lhs, *prod_len, *tok_off;
+    const uint8_t *bytes;
+    int32_t n_lex, n_lr, n_term, n_nt, end_term, eos, V;
+};
+
+constexpr int kAdvBlock = 64;          // sequences per workgroup (one per thread)
+constexpr int kOverlay = 192;          // states one token may push above what it keeps
+constexpr int kFeedSteps = 1 << 16;    // bound on the LR steps of one terminal
+
+// One thread advances one sequence by one token.  While the token is
+// processed the kept part of the stack, stacks[b][0 .. ptr), is only read and
+// the states pushed above it live in an LDS overlay, so a rejected token
+// leaves the stack, its length and the lexer state exactly as they were; on
+// success the overlay is written above ptr.  A terminal is fed as the LR
+// parser does: the reductions its lookahead selects, then a shift (accept
+// for $end); popping the whole stack or a missing goto rejects.
+__global__ void __launch_bounds__(kAdvBlock)
+advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ lens,
+               int32_t *__restrict__ qs, int32_t B, const int32_t *__restrict__ tokens,
+               int32_t *__restrict__ status) {
+    __shared__ int32_t s_ov[kOverlay][kAdvBlock];
+    const int b = blockIdx.x * kAdvBlock + threadIdx.x;
+    if (b >= B) return;
+    const int tok = tokens[b];
+    if (tok < 0) { status[b] = PSC_ADV_SKIPPED; return; }
+    const int len = lens[b], q_in = qs[b];
+    if (tok >= T.V || len < 1 || len > cap || q_in < 0 || q_in >= T.n_lex) {
+        status[b] = PSC_ADV_BAD_INPUT;
+        return;
+    }
+    const int32_t *st = stacks + (int64_t)b * cap;
+    int ptr = len, ov = 0;
+    auto top = [&]() { return ov > 0 ? s_ov[ov - 1][threadIdx.x] : st[ptr - 1]; };
+    auto push = [&](int32_t x) {
+        if (ov >= kOverlay) return false;
+        s_ov[ov++][threadIdx.x] = x;
+        return true;
+    };
+    // states come from the tables (validated when built) or, below the
+    // overlay, from the caller's stack, which is checked before each use
+    auto feed = [&](int32_t t) -> int {
+        for (int guard = 0; guard < kFeedSteps; guard++) {
+            const int32_t s0 = top();
+            if (s0 < 0 || s0 >= T.n_lr) return PSC_ADV_BAD_INPUT;
+            const int32_t a = T.action[(int64_t)s0 * T.n_term + t];
+            const int kind = a & 3;
+            if (kind == 1) return push(a >> 2) ? PSC_ADV_OK : PSC_ADV_OVERFLOW;
+            if (kind == 3) return PSC_ADV_OK;
+            if (kind == 0) return PSC_ADV_REJECTED;
+            const int32_t p = a >> 2;
+            int k = T.prod_len[p];
+            const int from_ov = min(k, ov);
+            ov -= from_ov;
+            k -= from_ov;
+            if (k >= ptr) return PSC_ADV_REJECTED;       // nothing left to goto from
+            ptr -= k;
+            const int32_t s1 = top();
+            if (s1 < 0 || s1 >= T.n_lr) return PSC_ADV_BAD_INPUT;
+            const int32_t g = T.go[(int64_t)s1 * T.n_nt + T.prod_lhs[p]];
+            if (g < 0) return PSC_ADV_REJECTED;
+            if (!push(g)) return PSC_ADV_OVERFLOW;
+        }
+        return PSC_ADV_REJECTED;
+    };
+    int q = q_in, res = PSC_ADV_OK;
+    if (tok == T.eos) {
+        // the pending lexeme becomes its terminal, then $end must be accepted
+        res = PSC_ADV_EOS;
+        if (q != 0) {
+            const int32_t t = T.lex_accept[q];
+            if (t < 0) res = PSC_ADV_REJECTED;
+            else if (!T.ignored[t]) {
+                const int r = feed(t);
+                if (r != PSC_ADV_OK) res = r;
+            }
+        }
+        if (res == PSC_ADV_EOS) {
+            const int r = feed(T.end_term);
+            if (r != PSC_ADV_OK) res = r;
+        }
+        status[b] = res;
+        return;
+    }
+    // longest match with one byte of lookahead: a byte the pending lexeme
+    // cannot take ends it (it must be accepting) and starts the next from q0
+    for (int i = T.tok_off[tok], e = T.tok_off[tok + 1]; i < e; i++) {
+        const int c = T.bytes[i];
+        const int32_t nx = T.lex_next[(int64_t)q * 256 + c];
+        if (nx >= 0) { q = nx; continue; }
+        const int32_t t = q != 0 ? T.lex_accept[q] : -1;
+        if (t < 0) { res = PSC_ADV_REJECTED; break; }
+        if (!T.ignored[t]) {
+            res = feed(t);
+            if (res != PSC_ADV_OK) break;
+        }
+        q = T.lex_next[c];
+        if (q < 0) { res = PSC_ADV_REJECTED; break; }
+    }
+    if (res == PSC_ADV_OK && ptr + ov > cap) res = PSC_ADV_OVERFLOW;
+    if (res == PSC_ADV_OK) {
+        int32_t *dst = stacks + (int64_t)b * cap + ptr;
+        for (int k = 0; k < ov; k++) dst[k] = s_ov[k][threadIdx.x];
+        lens[b] = ptr + ov;
+        qs[b] = q;
+    }
+    status[b] = res;
+}
+
+// Every sequence back to the empty prefix: lexer state q0, stack [0].
+__global__ void __launch_bounds__(kBlock)
+reset_kernel(int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ lens, int32_t *__restrict__ qs,
+             int32_t B) {
+    const int b = blockIdx.x * kBlock + threadIdx.x;
+    if (b >= B) return;
+    stacks[(int64_t)b * cap] = 0;
+    lens[b] = 1;
+    qs[b] = 0;
+}
+
 psc_status device_fail(const char *what, hipError_t e) {
     set_error(std::string(what) + ": " + hipGetErrorString(e));
     return PSC_E_DEVICE;
+}
+
+psc_status check_bound(const psc_handle *h, const char *what) {
+    if (!h) {
+        set_error(std::string(what) + ": null handle");
+        return PSC_E_INVALID_ARG;
+    }
+    if (!h->dev_base) {
+        set_error(std::string(what) + ": device tables not bound");
+        return PSC_E_NOT_BOUND;
+    }
+    return PSC_OK;
+}
+
+// The walk + gather kernel for ragged (stride 0) or strided stacks.
+psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
+                          const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *stream,
+                          const char *what) {
+    if (psc_status st = check_bound(h, what)) return st;
+    if (B < 0 || stride < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_bitmask))) {
+        set_error(std::string(what) + ": null argument or negative size");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B > 65535) {
+        set_error(std::string(what) + ": B > 65535");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    char *base = static_cast<char *>(h->dev_base);
+    const int32_t W = h->W;
+    const int vec4 = (W % 4 == 0) && ((reinterpret_cast<uintptr_t>(out_bitmask) & 15) == 0);
+    dim3 grid((W + kCopyWordsPerBlock - 1) / kCopyWordsPerBlock, B);
+    hipLaunchKernelGGL(walk_gather_kernel, grid, dim3(kBlock), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<const int32_t *>(base + kTableOff),
+                       reinterpret_cast<const uint32_t *>(base + h->mask_off), h->mask_stride, h->n_lex, h->n_lr,
+                       stacks, stride, stack_lens, lexer_states, B, W, out_bitmask,
+                       reinterpret_cast<uint32_t *>(base), vec4);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+}
+
+// The single-launch step for ragged (stride 0) or strided stacks.
+psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
+                        const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
+                        psc_dtype dtype, int32_t V, void *stream, const char *what) {
+    if (psc_status st = check_bound(h, what)) return st;
+    if (B < 0 || stride < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
+        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits))) {
+        set_error(std::string(what) + ": null argument, negative size or bad dtype");
+        return PSC_E_INVALID_ARG;
+    }
+    if (V != h->V) {
+        set_error(std::string(what) + ": V (" + std::to_string(V) + ") differs from the vocabulary size (" +
+                  std::to_string(h->V) + ")");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B > 65535) {
+        set_error(std::string(what) + ": B > 65535");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(h->dev_base);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
+    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const int32_t W = h->W;
+    const bool bf16 = dtype == PSC_BF16;
+    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    if (fast) {
+        const int words_per_block = (kBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
+                                                             : ApplyGeom<false>::kWordsPerWave);
+        dim3 grid((W + words_per_block - 1) / words_per_block, B);
+        if (bf16)
+            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
+                               reinterpret_cast<uint4 *>(logits));
+        else
+            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
+                               reinterpret_cast<uint4 *>(logits));
+    } else {
+        dim3 grid((W + kGenWords - 1) / kGenWords, B);
+        if (bf16)
+            hipLaunchKernelGGL(fused_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, out_bitmask,
+                               err, logits);
+        else
+            hipLaunchKernelGGL(fused_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
+                               h->mask_stride, h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W,
+                               out_bitmask, err, logits);
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+}
+
+psc_status check_dense(const int32_t *stacks, int32_t cap, const int32_t *lens, const int32_t *qs, int32_t B,
+                       const char *what) {
+    if (B < 0 || cap < 1 || (B > 0 && (!stacks || !lens || !qs))) {
+        set_error(std::string(what) + ": null argument, B < 0 or cap < 1");
+        return PSC_E_INVALID_ARG;
+    }
+    if ((int64_t)B * cap > ((int64_t)1 << 40)) {
+        set_error(std::string(what) + ": B * cap too large");
+        return PSC_E_INVALID_ARG;
+    }
+    return PSC_OK;
 }
 
 }  // namespace
@@ -399,51 +636,100 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
         set_error("psc_bind_device: buffer too small (" + std::to_string(nbytes) + " < " + std::to_string(need) + ")");
         return PSC_E_INVALID_ARG;
     }
+    auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(dev_buf);
-    size_t tb = (h->table.size() * sizeof(int32_t) + 255) & ~(size_t)255;
+    const size_t mask_off = kTableOff + up(h->table.size() * sizeof(int32_t));
+    const size_t gram_off = mask_off + up(h->masks.size() * sizeof(uint32_t));
+    const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
     hipError_t e = hipMemsetAsync(base, 0, kTableOff, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + kTableOff, h->table.data(), h->table.size() * sizeof(int32_t),
                            hipMemcpyHostToDevice, s);
     if (e == hipSuccess)
-        e = hipMemcpyAsync(base + kTableOff + tb, h->masks.data(), h->masks.size() * sizeof(uint32_t),
+        e = hipMemcpyAsync(base + mask_off, h->masks.data(), h->masks.size() * sizeof(uint32_t),
                            hipMemcpyHostToDevice, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(base + gram_off, h->gram.data(), h->gram.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(base + vbytes_off, h->vbytes.data(), h->vbytes.size(), hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return device_fail("psc_bind_device", e);
     h->dev_base = dev_buf;
     h->dev_bytes = nbytes;
-    h->mask_off = kTableOff + tb;
+    h->mask_off = mask_off;
+    h->gram_off = gram_off;
+    h->vbytes_off = vbytes_off;
     return PSC_OK;
 }
 
 extern "C" psc_status psc_compute_masks(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                         const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
                                         void *stream) {
-    if (!h || B < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_bitmask))) {
-        set_error("psc_compute_masks: null argument or B < 0");
-        return PSC_E_INVALID_ARG;
-    }
-    if (!h->dev_base) {
-        set_error("psc_compute_masks: device tables not bound");
-        return PSC_E_NOT_BOUND;
-    }
-    if (B > 65535) {
-        set_error("psc_compute_masks: B > 65535");
+    return launch_compute(h, stacks, 0, stack_lens, lexer_states, B, out_bitmask, stream, "psc_compute_masks");
+}
+
+extern "C" psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                            const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
+                                            void *logits, psc_dtype dtype, int32_t V, void *stream) {
+    return launch_fused(h, stacks, 0, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
+                        "psc_compute_and_apply");
+}
+
+extern "C" psc_status psc_compute_masks_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                              const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                              uint32_t *out_bitmask, void *stream) {
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_masks_dense")) return st;
+    return launch_compute(h, stacks, cap, stack_lens, lexer_states, B, out_bitmask, stream,
+                          "psc_compute_masks_dense");
+}
+
+extern "C" psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                                  const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                                  uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                                  void *stream) {
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_and_apply_dense"))
+        return st;
+    return launch_fused(h, stacks, cap, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
+                        "psc_compute_and_apply_dense");
+}
+
+extern "C" psc_status psc_state_reset(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,
+                                      int32_t *lexer_states, int32_t B, void *stream) {
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_state_reset")) return st;
+    if (!h) {
+        set_error("psc_state_reset: null handle");
         return PSC_E_INVALID_ARG;
     }
     if (B == 0) return PSC_OK;
-    char *base = static_cast<char *>(h->dev_base);
-    const int32_t W = h->W;
-    const int vec4 = (W % 4 == 0) && ((reinterpret_cast<uintptr_t>(out_bitmask) & 15) == 0);
-    dim3 grid((W + kCopyWordsPerBlock - 1) / kCopyWordsPerBlock, B);
-    hipLaunchKernelGGL(walk_gather_kernel, grid, dim3(kBlock), 0, reinterpret_cast<hipStream_t>(stream),
-                       reinterpret_cast<const int32_t *>(base + kTableOff),
-                       reinterpret_cast<const uint32_t *>(base + h->mask_off), h->mask_stride, h->n_lex, h->n_lr,
-                       stacks, stack_lens, lexer_states, B, W, out_bitmask, reinterpret_cast<uint32_t *>(base),
-                       vec4);
+    hipLaunchKernelGGL(reset_kernel, dim3((B + kBlock - 1) / kBlock), dim3(kBlock), 0,
+                       reinterpret_cast<hipStream_t>(stream), stacks, cap, stack_lens, lexer_states, B);
     hipError_t e = hipGetLastError();
-    return e == hipSuccess ? PSC_OK : device_fail("psc_compute_masks", e);
+    return e == hipSuccess ? PSC_OK : device_fail("psc_state_reset", e);
+}
+
+extern "C" psc_status psc_advance(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,
+                                  int32_t *lexer_states, int32_t B, const int32_t *tokens, int32_t *status,
+                                  void *stream) {
+    if (psc_status st = check_bound(h, "psc_advance")) return st;
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_advance")) return st;
+    if (B > 0 && (!tokens || !status)) {
+        set_error("psc_advance: null tokens or status");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    const char *base = static_cast<const char *>(h->dev_base);
+    const int32_t *g = reinterpret_cast<const int32_t *>(base + h->gram_off);
+    const psc::AdvanceLayout &L = h->adv;
+    AdvTables T{g + L.lex_next, g + L.lex_accept, g + L.ignored, g + L.action, g + L.go, g + L.prod_lhs,
+                g + L.prod_len, g + L.tok_off, reinterpret_cast<const uint8_t *>(base + h->vbytes_off),
+                h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V};
+    hipLaunchKernelGGL(advance_kernel, dim3((B + kAdvBlock - 1) / kAdvBlock), dim3(kAdvBlock), 0,
+                       reinterpret_cast<hipStream_t>(stream), T, stacks, cap, stack_lens, lexer_states, B, tokens,
+                       status);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail("psc_advance", e);
 }
 
 extern "C" psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask, int32_t B, int32_t V,
@@ -504,60 +790,4 @@ extern "C" psc_status psc_device_error_count(const psc_handle *h, uint32_t *out,
     if (e == hipSuccess && reset) e = hipMemsetAsync(h->dev_base, 0, sizeof(uint32_t), s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     return e == hipSuccess ? PSC_OK : device_fail("psc_device_error_count", e);
-}
-
-extern "C" psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
-                                            const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
-                                            void *logits, psc_dtype dtype, int32_t V, void *stream) {
-    if (!h || B < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
-        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits))) {
-        set_error("psc_compute_and_apply: null argument, B < 0 or bad dtype");
-        return PSC_E_INVALID_ARG;
-    }
-    if (V != h->V) {
-        set_error("psc_compute_and_apply: V (" + std::to_string(V) + ") differs from the vocabulary size (" +
-                  std::to_string(h->V) + ")");
-        return PSC_E_INVALID_ARG;
-    }
-    if (!h->dev_base) {
-        set_error("psc_compute_and_apply: device tables not bound");
-        return PSC_E_NOT_BOUND;
-    }
-    if (B > 65535) {
-        set_error("psc_compute_and_apply: B > 65535");
-        return PSC_E_INVALID_ARG;
-    }
-    if (B == 0) return PSC_OK;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
-    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
-    uint32_t *err = reinterpret_cast<uint32_t *>(base);
-    const int32_t W = h->W;
-    const bool bf16 = dtype == PSC_BF16;
-    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
-    if (fast) {
-        const int words_per_block = (kBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
-                                                             : ApplyGeom<false>::kWordsPerWave);
-        dim3 grid((W + words_per_block - 1) / words_per_block, B);
-        if (bf16)
-            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, W, out_bitmask, err,
-                               reinterpret_cast<uint4 *>(logits));
-        else
-            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, W, out_bitmask, err,
-                               reinterpret_cast<uint4 *>(logits));
-    } else {
-        dim3 grid((W + kGenWords - 1) / kGenWords, B);
-        if (bf16)
-            hipLaunchKernelGGL(fused_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, V, W, out_bitmask, err, logits);
-        else
-            hipLaunchKernelGGL(fused_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
-                               h->mask_stride, h->n_lex, h->n_lr, stacks, stack_lens, lexer_states, V, W,
-                               out_bitmask, err, logits);
-    }
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? PSC_OK : device_fail("psc_compute_and_apply", e);
 }

@@ -51,10 +51,26 @@ inline bool ref_is_dense(int32_t ref) { return (ref & 3) == kRefDense; }
 inline bool ref_is_chain(int32_t ref) { return (ref & 3) == kRefChain; }
 inline int32_t ref_offset(int32_t ref) { return ref & ~3; }
 
+// The problem instance as the device advance of prefix states reads it: one
+// int32 blob, sections at these int32 offsets, plus the vocabulary bytes.
+struct AdvanceLayout {
+    int64_t lex_next = 0;   // [n_lex][256]
+    int64_t lex_accept = 0; // [n_lex]
+    int64_t ignored = 0;    // [n_term] 0/1
+    int64_t action = 0;     // [n_lr][n_term]
+    int64_t go = 0;         // [n_lr][n_nt]
+    int64_t prod_lhs = 0;   // [n_prod]
+    int64_t prod_len = 0;   // [n_prod]
+    int64_t tok_off = 0;    // [V + 1] byte offsets of the spellings
+    int32_t n_term = 0, n_nt = 0, end_term = 0, eos = -1;
+};
+
 // Device buffer layout (offsets in bytes from the bound base):
 //   [0, 256)                   uint32 error counter (+ padding)
 //   [kTableOff, ...)           int32 table: start refs [n_lex], rows, pad
 //   [mask_off, ...)            uint32 masks [n_classes][mask_stride] (256-B aligned)
+//   [gram_off, ...)            int32 advance blob (AdvanceLayout)
+//   [vbytes_off, ...)          uint8 vocabulary bytes
 constexpr size_t kTableOff = 256;
 
 }  // namespace psc
@@ -63,11 +79,14 @@ struct psc_handle {
     int32_t V = 0, W = 0, mask_stride = 0, n_lex = 0, n_lr = 0, n_classes = 0;
     std::vector<int32_t> table;    // start refs then rows then padding
     std::vector<uint32_t> masks;   // [n_classes][mask_stride]
+    std::vector<int32_t> gram;     // advance blob
+    std::vector<uint8_t> vbytes;   // vocabulary bytes (at least 1)
+    psc::AdvanceLayout adv;
     psc_info_t info{};
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
-    size_t mask_off = 0;
+    size_t mask_off = 0, gram_off = 0, vbytes_off = 0;
     size_t device_bytes_needed() const;
 };
 

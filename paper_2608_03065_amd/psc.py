@@ -15,11 +15,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpsc.so")
 
 PSC_F32, PSC_BF16 = 0, 1
+ADV_OK, ADV_REJECTED, ADV_EOS, ADV_OVERFLOW, ADV_BAD_INPUT, ADV_SKIPPED = range(6)
 _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E_OOM",
            -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT"}
 
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
-            "psc_apply_mask", "psc_compute_and_apply", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
+            "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -78,6 +80,10 @@ def lib() -> C.CDLL:
         L.psc_compute_masks.argtypes = [P, P, P, P, I32, P, P]
         L.psc_apply_mask.argtypes = [P, C.c_int, P, I32, I32, P]
         L.psc_compute_and_apply.argtypes = [P, P, P, P, I32, P, P, C.c_int, I32, P]
+        L.psc_state_reset.argtypes = [P, P, I32, P, P, I32, P]
+        L.psc_advance.argtypes = [P, P, I32, P, P, I32, P, P, P]
+        L.psc_compute_masks_dense.argtypes = [P, P, I32, P, P, I32, P, P]
+        L.psc_compute_and_apply_dense.argtypes = [P, P, I32, P, P, I32, P, P, C.c_int, I32, P]
         L.psc_device_error_count.argtypes = [P, P, I32, P]
         L.psc_classify_host.argtypes = [P, P, P, P, I32, P]
         L.psc_class_mask_host.argtypes = [P, I32, P]
@@ -85,7 +91,8 @@ def lib() -> C.CDLL:
         L.psc_free.restype = None
         L.psc_last_error.restype = C.c_char_p
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
-                     "psc_compute_and_apply", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
+                     "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
+                     "psc_compute_and_apply_dense", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -227,6 +234,78 @@ class Classifier:
         v = C.c_uint32()
         _check(lib().psc_device_error_count(self._h, C.byref(v), int(reset), _stream_ptr(stream)))
         return int(v.value)
+
+
+class DecodeStates:
+    """B device-resident prefix states in the dense layout of psc_advance:
+    stacks int32 [B, cap], lens int32 [B], qs int32 [B] (torch tensors)."""
+
+    def __init__(self, clf: Classifier, B: int, cap: int, device="cuda", stream=None):
+        import torch
+        self.clf, self.B, self.cap = clf, int(B), int(cap)
+        self.stacks = torch.zeros((self.B, self.cap), dtype=torch.int32, device=device)
+        self.lens = torch.zeros(self.B, dtype=torch.int32, device=device)
+        self.qs = torch.zeros(self.B, dtype=torch.int32, device=device)
+        self.status = torch.zeros(self.B, dtype=torch.int32, device=device)
+        self.reset(stream)
+
+    def reset(self, stream=None):
+        """Every sequence to the empty prefix (q0, stack [0])."""
+        _check(lib().psc_state_reset(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
+                                     self.qs.data_ptr(), self.B, _stream_ptr(stream)))
+        return self
+
+    def load(self, states):
+        """Set the states from host (q, stack bottom->top) pairs."""
+        import torch
+        assert len(states) == self.B
+        st = np.zeros((self.B, self.cap), np.int32)
+        for b, (q, a) in enumerate(states):
+            assert 1 <= len(a) <= self.cap
+            st[b, :len(a)] = a
+        self.stacks.copy_(torch.from_numpy(st))
+        self.lens.copy_(torch.tensor([len(a) for _, a in states], dtype=torch.int32))
+        self.qs.copy_(torch.tensor([q for q, _ in states], dtype=torch.int32))
+        return self
+
+    def advance(self, tokens, stream=None):
+        """One token per sequence (int32 device tensor [B], < 0 = skip);
+        returns the status tensor (ADV_*)."""
+        import torch
+        assert tokens.is_cuda and tokens.dtype == torch.int32 and tokens.numel() == self.B
+        _check(lib().psc_advance(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
+                                 self.qs.data_ptr(), self.B, tokens.data_ptr(), self.status.data_ptr(),
+                                 _stream_ptr(stream)))
+        return self.status
+
+    def compute_masks(self, out=None, stream=None):
+        import torch
+        if out is None:
+            out = torch.empty((self.B, self.clf.W), dtype=torch.int32, device=self.lens.device)
+        assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
+        _check(lib().psc_compute_masks_dense(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
+                                             self.qs.data_ptr(), self.B, out.data_ptr(), _stream_ptr(stream)))
+        return out
+
+    def compute_and_apply(self, logits, out=None, stream=None):
+        import torch
+        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
+        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        out_ptr = None
+        if out is not None:
+            assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
+            out_ptr = out.data_ptr()
+        _check(lib().psc_compute_and_apply_dense(self.clf._h, self.stacks.data_ptr(), self.cap,
+                                                 self.lens.data_ptr(), self.qs.data_ptr(), self.B, out_ptr,
+                                                 logits.data_ptr(), dt, self.clf.V, _stream_ptr(stream)))
+        return logits
+
+    def host_states(self):
+        """The states as host (q, stack) pairs (synchronises)."""
+        st = self.stacks.cpu().numpy()
+        lens = self.lens.cpu().numpy()
+        qs = self.qs.cpu().numpy()
+        return [(int(qs[b]), st[b, :lens[b]].copy()) for b in range(self.B)]
 
 
 def apply_mask(logits, bitmask, stream=None):

@@ -213,17 +213,5 @@ def json_accepts(s: bytes) -> bool:
 
 def greedy_tokenize(text: bytes, tokens: list[bytes], eos_id: int) -> list[int]:
     """Longest-match tokenisation over a vocabulary (teacher forcing)."""
-    index: dict[bytes, int] = {t: i for i, t in enumerate(tokens) if i != eos_id and t}
-    maxlen = max(len(t) for t in index)
-    out = []
-    i = 0
-    while i < len(text):
-        for L in range(min(maxlen, len(text) - i), 0, -1):
-            j = index.get(text[i:i + L])
-            if j is not None:
-                out.append(j)
-                i += L
-                break
-        else:
-            raise ValueError("text not coverable by the vocabulary")
-    return out
+    from inputs.vocab import Vocab
+    return Vocab(list(tokens), eos_id).tokenize(text)

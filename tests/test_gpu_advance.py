@@ -1,0 +1,146 @@
+"""GPU parity of the device-resident prefix states through the C-ABI:
+psc_advance against the oracle's one-token advance (status, lexer state and
+stack, exactly), and the dense-layout masks against the oracle's masks."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from inputs.seeds import rng_for  # noqa: E402
+from oracle import Oracle  # noqa: E402
+from paper_2608_03065_amd import psc  # noqa: E402
+from paper_2608_03065_amd.psc import DecodeStates, apply_mask, pack_states  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _oracle_step(orc, states, toks, cap):
+    """Expected (status, states) after one token per sequence."""
+    status, out = [], []
+    for st, t in zip(states, toks):
+        if t < 0:
+            status.append(psc.ADV_SKIPPED)
+            out.append(st)
+            continue
+        code, new = orc.advance(st, int(t), cap)
+        status.append(code)
+        out.append(new if code == Oracle.ADVANCED else st)
+    return np.array(status, np.int32), out
+
+
+def _same_states(got, want):
+    for b, ((q1, s1), (q2, s2)) in enumerate(zip(got, want)):
+        if q1 != q2 or not np.array_equal(s1, s2):
+            return b
+    return -1
+
+
+@pytest.mark.parametrize("name,B,n_tok", [("arithmetic", 24, 80), ("json", 16, 120), ("schema", 8, 160),
+                                          ("pylike", 6, 120)])
+def test_advance_documents(built, name, B, n_tok):
+    """B documents fed token by token (then EOS, then skips), every step
+    compared with the oracle."""
+    wl, clf, orc = built(name)
+    cap = 4096
+    docs = [wl.make_document(rng_for(wl.index, 91, b, salt=0xADD), wl) for b in range(B)]
+    seqs = [wl.vocab.tokenize(d)[:n_tok] for d in docs]
+    full = [len(wl.vocab.tokenize(d)) <= n_tok for d in docs]
+    ds = DecodeStates(clf, B, cap, DEV)
+    want = ds.host_states()
+    for k in range(n_tok + 2):
+        toks = []
+        for b in range(B):
+            if k < len(seqs[b]):
+                toks.append(seqs[b][k])
+            elif k == len(seqs[b]) and full[b]:
+                toks.append(wl.vocab.eos_id)
+            else:
+                toks.append(-1)
+        toks = np.array(toks, np.int32)
+        st = ds.advance(torch.from_numpy(toks).to(DEV)).cpu().numpy()
+        exp_st, want = _oracle_step(orc, want, toks, cap)
+        assert np.array_equal(st, exp_st), (k, np.nonzero(st != exp_st)[0][:5])
+        bad = _same_states(ds.host_states(), want)
+        assert bad < 0, (k, bad)
+    assert (st == psc.ADV_SKIPPED).all()
+
+
+@pytest.mark.parametrize("name", ["arithmetic", "json", "schema"])
+def test_advance_random_tokens(built, name):
+    """Mostly invalid tokens from mid-document states: rejections leave the
+    state untouched, acceptances match the oracle."""
+    wl, clf, orc = built(name)
+    rng = np.random.default_rng(11)
+    states = wl.states(17, B=64)
+    cap = max(len(a) for _, a in states) + 64
+    ds = DecodeStates(clf, 64, cap, DEV).load(states)
+    want = states
+    for k in range(6):
+        toks = rng.integers(0, wl.V, 64).astype(np.int32)
+        toks[::7] = wl.vocab.eos_id
+        st = ds.advance(torch.from_numpy(toks).to(DEV)).cpu().numpy()
+        exp_st, want = _oracle_step(orc, want, toks, cap)
+        assert np.array_equal(st, exp_st), k
+        assert _same_states(ds.host_states(), want) < 0, k
+
+
+def test_advance_limits(built):
+    wl, clf, orc = built("arithmetic")
+    toks = wl.vocab.tokens
+    lp = toks.index(b"(")
+    ds = DecodeStates(clf, 4, 3, DEV)
+    # "(" x4 with cap 3: the stack grows by one per "(" after the first
+    t = torch.full((4,), lp, dtype=torch.int32, device=DEV)
+    codes = [ds.advance(t).cpu().numpy().tolist() for _ in range(4)]
+    assert codes[0] == [psc.ADV_OK] * 4
+    assert codes[-1] == [psc.ADV_OVERFLOW] * 4
+    lens = ds.lens.cpu().numpy()
+    assert (lens <= 3).all()
+    before = ds.host_states()
+    bad = torch.tensor([wl.V, -1, -5, lp], dtype=torch.int32, device=DEV)
+    st = ds.advance(bad).cpu().numpy()
+    assert st[0] == psc.ADV_BAD_INPUT and st[1] == psc.ADV_SKIPPED and st[2] == psc.ADV_SKIPPED
+    assert _same_states(ds.host_states()[:3], before[:3]) < 0
+    # a lexer state out of range is bad input too
+    ds.qs[0] = wl.grammar.lexer.n_states
+    st = ds.advance(torch.full((4,), lp, dtype=torch.int32, device=DEV)).cpu().numpy()
+    assert st[0] == psc.ADV_BAD_INPUT
+
+
+@pytest.mark.parametrize("name,B,steps", [("json", 32, 40), ("schema", 64, 40), ("pylike", 32, 30)])
+def test_masked_decoding_loop(built, name, B, steps):
+    """A decoding loop run entirely on device states: masks (dense), a seeded
+    choice among the allowed tokens, advance.  Every allowed token advances;
+    the dense masks equal the oracle's and the ragged path's; the fused dense
+    step applies them to the logits exactly."""
+    wl, clf, orc = built(name)
+    rng = np.random.default_rng(3)
+    cap = 1024
+    ds = DecodeStates(clf, B, cap, DEV)
+    eos = wl.vocab.eos_id
+    for k in range(steps):
+        bm = ds.compute_masks().cpu().numpy().view(np.uint32)
+        states = ds.host_states()
+        if k % 10 == 0:
+            assert np.array_equal(bm, orc.masks(states)), k
+            stacks, lens, qs = pack_states(states, DEV)
+            assert np.array_equal(clf.compute_masks(stacks, lens, qs).cpu().numpy().view(np.uint32), bm)
+            logits = wl.logits(k, B=B)
+            dev = logits.to(DEV)
+            out = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
+            ds.compute_and_apply(dev, out=out)
+            two = logits.to(DEV)
+            apply_mask(two, torch.from_numpy(bm.view(np.int32)).to(DEV))
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy().view(np.uint32), bm)
+            assert torch.equal(dev.cpu(), two.cpu())
+        toks = np.full(B, -1, np.int32)
+        for b in range(B):
+            allowed = np.nonzero(np.unpackbits(bm[b].astype("<u4").view(np.uint8), bitorder="little")[:wl.V])[0]
+            allowed = allowed[allowed != eos]
+            if allowed.size:
+                toks[b] = rng.choice(allowed)
+        st = ds.advance(torch.from_numpy(toks).to(DEV)).cpu().numpy()
+        assert ((st == psc.ADV_OK) | (toks < 0)).all(), (k, st[(st != psc.ADV_OK) & (toks >= 0)][:5])
+    assert clf.error_count() == 0

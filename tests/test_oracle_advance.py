@@ -14,11 +14,10 @@ import pytest
 from inputs import configs
 from inputs.seeds import rng_for
 from oracle import Oracle
-from tests.recognizers import greedy_tokenize
 
 
 def _walk_document(wl, orc, text):
-    toks = greedy_tokenize(text, wl.vocab.tokens, wl.vocab.eos_id)
+    toks = wl.vocab.tokenize(text)
     cuts = np.cumsum([len(wl.vocab.tokens[t]) for t in toks])
     want = wl.host.states_at(text, cuts)
     state = wl.host.state(b"")
