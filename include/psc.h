@@ -39,7 +39,10 @@ typedef enum {
     PSC_E_OOM = -4,         /* host allocation failed                                 */
     PSC_E_DEVICE = -5,      /* a HIP call or kernel launch failed                     */
     PSC_E_NOT_BOUND = -6,   /* device tables not bound (psc_bind_device)              */
-    PSC_E_LIMIT = -7        /* the construction exceeded a size limit                 */
+    PSC_E_LIMIT = -7,       /* the construction exceeded a size limit                 */
+    PSC_E_IO = -8,          /* a file could not be opened, read or written            */
+    PSC_E_FORMAT = -9       /* not a classifier file, unsupported version, corrupt or
+                               inconsistent contents                                    */
 } psc_status;
 
 typedef enum { PSC_F32 = 0, PSC_BF16 = 1 } psc_dtype;
@@ -125,6 +128,23 @@ typedef struct {
  * an empty spelling), PSC_E_OOM, PSC_E_LIMIT.
  */
 psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out);
+
+/*
+ * Persistence of a built classifier, so that Algorithm 1 runs once per
+ * (grammar, vocabulary) pair (the preprocessing the paper stores, Sec. 4 /
+ * Tab. preprocess).  psc_save writes everything a handle holds (classifier
+ * table, mask table, and the lexer, parser and vocabulary psc_advance reads)
+ * to `path`, each part checksummed, the large ones deflate-compressed.
+ * psc_load reads such a file into a new, unbound handle.  A loaded file is
+ * untrusted: psc_load verifies the checksums and the structure the device
+ * kernels rely on (every ref names a row, a chain entry of the right kind or
+ * a class; chains end within one wavefront load; the lexer, parser and
+ * vocabulary pass psc_build's input checks) before it returns a handle.
+ * Files are little-endian and tied to this library's format version.
+ * Errors: PSC_E_INVALID_ARG, PSC_E_IO, PSC_E_FORMAT, PSC_E_OOM.
+ */
+psc_status psc_save(const psc_handle *h, const char *path);
+psc_status psc_load(const char *path, psc_handle **out);
 
 /* Sizes and statistics of a built handle. */
 psc_status psc_info(const psc_handle *h, psc_info_t *out);

@@ -1,4 +1,5 @@
-"""Build libpsc.so in-tree: host construction (g++) + gfx950 device code (hipcc)."""
+"""Build libpsc.so in-tree: host construction and persistence (g++, zlib) +
+gfx950 device code (hipcc)."""
 from __future__ import annotations
 
 import os
@@ -32,10 +33,12 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     host_obj = os.path.join(BUILD_DIR, "psc_build.o")
     dev_obj = os.path.join(BUILD_DIR, "psc_device.o")
+    store_obj = os.path.join(BUILD_DIR, "psc_store.o")
     _run(["g++", *HOST_FLAGS, f"-I{ROCM}/include", "-c", os.path.join(CSRC, "psc_build.cpp"), "-o", host_obj])
+    _run(["g++", *HOST_FLAGS, f"-I{ROCM}/include", "-c", os.path.join(CSRC, "psc_store.cpp"), "-o", store_obj])
     _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, "psc_device.hip"), "-o", dev_obj])
     tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", host_obj, dev_obj, "-o", tmp])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", host_obj, store_obj, dev_obj, "-lz", "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -900,6 +900,16 @@ std::vector<int32_t> minimise(const Automaton &B, int32_t *n_blocks_out) {
 }
 
 }  // namespace
+
+psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg) {
+    try {
+        validate(g, v);
+        return PSC_OK;
+    } catch (const BuildError &e) {
+        *msg = e.what();
+        return e.code;
+    }
+}
 }  // namespace psc
 
 using namespace psc;
@@ -1140,6 +1150,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             }
         }
         int64_t off = (G.nQ + 3) & ~3;
+        h->rows_off = off;
         int32_t rows = 0, dense = 0, max_sparse = 0, chain_states = 0;
         for (int32_t b : order) {
             if (det[b] >= 0) { ref[b] = class_ref(det[b]); continue; }
@@ -1153,12 +1164,14 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             if (is_dense) dense++; else max_sparse = std::max(max_sparse, ne);
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
         }
+        h->chains_off = off;
         for (const auto &ch : chains) {
             for (size_t j = 0; j < ch.size(); j++) ref[ch[j]] = (int32_t)(off + kChainEntry * j) | kRefChain;
             off += kChainEntry * (int64_t)(ch.size() + 1);
             chain_states += (int32_t)ch.size();
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
         }
+        h->table_end = off;
         h->table.assign((size_t)off + kTablePad, 0);
         for (int32_t q = 0; q < G.nQ; q++) h->table[q] = ref[block[B.start_state[q]]];
         for (int32_t b : order) {

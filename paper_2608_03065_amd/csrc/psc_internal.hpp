@@ -77,7 +77,8 @@ constexpr size_t kTableOff = 256;
 
 struct psc_handle {
     int32_t V = 0, W = 0, mask_stride = 0, n_lex = 0, n_lr = 0, n_classes = 0;
-    std::vector<int32_t> table;    // start refs then rows then padding
+    std::vector<int32_t> table;    // start refs, rows, chains, padding
+    int64_t rows_off = 0, chains_off = 0, table_end = 0;   // regions of the table (int32 offsets)
     std::vector<uint32_t> masks;   // [n_classes][mask_stride]
     std::vector<int32_t> gram;     // advance blob
     std::vector<uint8_t> vbytes;   // vocabulary bytes (at least 1)
@@ -92,4 +93,6 @@ struct psc_handle {
 
 namespace psc {
 void set_error(const std::string &msg);
+// The input checks of psc_build (ids in range, spellings), for loaded tables.
+psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg);
 }

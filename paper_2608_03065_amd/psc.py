@@ -17,11 +17,12 @@ LIB_PATH = os.path.join(_HERE, "libpsc.so")
 PSC_F32, PSC_BF16 = 0, 1
 ADV_OK, ADV_REJECTED, ADV_EOS, ADV_OVERFLOW, ADV_BAD_INPUT, ADV_SKIPPED = range(6)
 _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E_OOM",
-           -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT"}
+           -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT", -8: "PSC_E_IO", -9: "PSC_E_FORMAT"}
 
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
             "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
-            "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_save", "psc_load",
+            "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -80,6 +81,8 @@ def lib() -> C.CDLL:
         L.psc_compute_masks.argtypes = [P, P, P, P, I32, P, P]
         L.psc_apply_mask.argtypes = [P, C.c_int, P, I32, I32, P]
         L.psc_compute_and_apply.argtypes = [P, P, P, P, I32, P, P, C.c_int, I32, P]
+        L.psc_save.argtypes = [P, C.c_char_p]
+        L.psc_load.argtypes = [C.c_char_p, C.POINTER(P)]
         L.psc_state_reset.argtypes = [P, P, I32, P, P, I32, P]
         L.psc_advance.argtypes = [P, P, I32, P, P, I32, P, P, P]
         L.psc_compute_masks_dense.argtypes = [P, P, I32, P, P, I32, P, P]
@@ -92,7 +95,8 @@ def lib() -> C.CDLL:
         L.psc_last_error.restype = C.c_char_p
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
-                     "psc_compute_and_apply_dense", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host"):
+                     "psc_compute_and_apply_dense", "psc_save", "psc_load", "psc_device_error_count",
+                     "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -125,7 +129,23 @@ def pack_states(states, device=None):
 
 
 class Classifier:
-    """A built (grammar, vocabulary) classifier: psc_build .. psc_free."""
+    """A built (grammar, vocabulary) classifier: psc_build .. psc_free; or one
+    read back with Classifier.load(path)."""
+
+    @classmethod
+    def load(cls, path: str) -> "Classifier":
+        h = C.c_void_p()
+        _check(lib().psc_load(os.fsencode(path), C.byref(h)))
+        self = cls.__new__(cls)
+        self._h = h
+        self._dev = None
+        inf = self.info()
+        self.V = inf["vocab_size"]
+        self.W = inf["mask_words"]
+        return self
+
+    def save(self, path: str) -> None:
+        _check(lib().psc_save(self._h, os.fsencode(path)))
 
     def __init__(self, grammar, vocab):
         g = grammar

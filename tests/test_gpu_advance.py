@@ -144,3 +144,32 @@ def test_masked_decoding_loop(built, name, B, steps):
         st = ds.advance(torch.from_numpy(toks).to(DEV)).cpu().numpy()
         assert ((st == psc.ADV_OK) | (toks < 0)).all(), (k, st[(st != psc.ADV_OK) & (toks >= 0)][:5])
     assert clf.error_count() == 0
+
+
+def test_loaded_classifier_on_device(built, tmp_path):
+    """psc_save then psc_load: the loaded handle, bound to the device, gives
+    the same masks, fused step and advances as the built one."""
+    from paper_2608_03065_amd.psc import Classifier
+    wl, clf, orc = built("schema")
+    path = str(tmp_path / "schema.psc")
+    clf.save(path)
+    back = Classifier.load(path).bind(DEV)
+    states = wl.states(21)
+    stacks, lens, qs = pack_states(states, DEV)
+    m1 = clf.compute_masks(stacks, lens, qs)
+    m2 = back.compute_masks(stacks, lens, qs)
+    logits = wl.logits(21)
+    l1, l2 = logits.to(DEV), logits.to(DEV)
+    clf.compute_and_apply(stacks, lens, qs, l1)
+    back.compute_and_apply(stacks, lens, qs, l2)
+    torch.cuda.synchronize()
+    assert torch.equal(m1, m2) and torch.equal(l1.view(torch.int16), l2.view(torch.int16))
+    assert np.array_equal(m2.cpu().numpy().view(np.uint32), orc.masks(states))
+    cap = max(len(a) for _, a in states) + 32
+    d1 = DecodeStates(clf, len(states), cap, DEV).load(states)
+    d2 = DecodeStates(back, len(states), cap, DEV).load(states)
+    rng = np.random.default_rng(2)
+    for _ in range(4):
+        t = torch.from_numpy(rng.integers(0, wl.V, len(states)).astype(np.int32)).to(DEV)
+        assert torch.equal(d1.advance(t), d2.advance(t))
+        assert _same_states(d1.host_states(), d2.host_states()) < 0
