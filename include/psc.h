@@ -214,6 +214,21 @@ psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, con
                                  psc_dtype dtype, int32_t V, void *stream);
 
 /*
+ * Greedy decoding folded into the mask step (the mask decides which logits
+ * sampling may see, Sec. 1 / Fig. 1a): for every sequence, the walk and then
+ *   out_tokens[b] = argmax over allowed tokens v of logits[b][v]
+ * (device int32 [B]): ties go to the lowest id, a NaN logit counts above
+ * every number, -0 equals +0, and a row with no allowed token (or a rejected
+ * input, as in psc_compute_masks) gives -1.  The logits (device, contiguous
+ * [B][V] of `dtype`, V = the vocabulary size) are only read, and only the
+ * 16-byte groups that hold an allowed token.  Errors: PSC_E_INVALID_ARG,
+ * PSC_E_NOT_BOUND, PSC_E_DEVICE.
+ */
+psc_status psc_compute_and_argmax(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                  const int32_t *lexer_states, int32_t B, const void *logits, psc_dtype dtype,
+                                  int32_t V, int32_t *out_tokens, void *stream);
+
+/*
  * Device-resident prefix states (Sec. 3.2: a prefix is represented by its
  * lexer state and parser stack; Algorithm 2 lexes and parses each new token
  * before classifying).  B sequences keep their states in HBM between decoding
@@ -272,6 +287,12 @@ psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stack
                                        const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
                                        uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
                                        void *stream);
+
+/* psc_compute_and_argmax on device-resident states (dense layout above). */
+psc_status psc_compute_and_argmax_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                        const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                        const void *logits, psc_dtype dtype, int32_t V, int32_t *out_tokens,
+                                        void *stream);
 
 /* Read (synchronously, on `stream`) and optionally reset the device counter
  * of sequences that psc_compute_masks rejected as out of range. */

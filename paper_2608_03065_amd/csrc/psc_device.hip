@@ -388,6 +388,96 @@ fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restri
     }
 }
 
+// ---------------------------------------------------------------- masked argmax
+
+// Greedy decoding folded into the mask step: out[b] = the allowed token with
+// the largest logit (ties to the lowest id; NaN above everything; -1 if no
+// token is allowed).  The logits are only read, and only the 16-byte vectors
+// holding at least one allowed token.  One workgroup per sequence walks once
+// and sweeps its whole row, so no reduction crosses workgroups.
+constexpr int kArgBlock = 1024;
+
+// An order-preserving key: larger float, larger key; NaN above +inf; -0 = +0.
+__device__ __forceinline__ uint32_t order_key(uint32_t u) {
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0xFFFFFFFFu;
+    if (u == 0x80000000u) u = 0;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ unsigned long long arg_key(uint32_t fbits, int v) {
+    return ((unsigned long long)order_key(fbits) << 32) | (0xFFFFFFFFu - (uint32_t)v);
+}
+
+template <bool kBf16>
+__global__ void __launch_bounds__(kArgBlock)
+argmax_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+              int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
+              const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
+              uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
+              int32_t *__restrict__ out) {
+    using G = ApplyGeom<kBf16>;
+    __shared__ unsigned long long s_best[kArgBlock / kWave];
+    const int b = blockIdx.y;
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    unsigned long long best = 0;   // every real key is > 0
+    if (cls >= 0) {
+        const uint32_t *mrow = masks + (size_t)cls * mask_stride;
+        if (fast) {
+            // the apply's layout: a wavefront takes kWordsPerWave words, lane j
+            // the vectors j, j + 64, ...; only vectors with an allowed token are read
+            const uint4 *row = reinterpret_cast<const uint4 *>(logits) + (size_t)b * W * G::kVecsPerWord;
+            constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
+            for (int w0 = wave * G::kWordsPerWave; w0 < W; w0 += (kArgBlock / kWave) * G::kWordsPerWave) {
+                const uint32_t m = lane < G::kWordsPerWave && w0 + lane < W ? mrow[w0 + lane] : 0u;
+                uint32_t g[G::kVecs];
+                uint4 x[G::kVecs];
+#pragma unroll
+                for (int j = 0; j < G::kVecs; j++) {
+                    const int v = j * kWave + lane;
+                    g[j] = (__shfl(m, v / G::kVecsPerWord, kWave) >> ((v % G::kVecsPerWord) * G::kPerVec)) & kFull;
+                }
+#pragma unroll
+                for (int j = 0; j < G::kVecs; j++)
+                    if (g[j]) x[j] = load_nt(row + (size_t)w0 * G::kVecsPerWord + j * kWave + lane);
+#pragma unroll
+                for (int j = 0; j < G::kVecs; j++) {
+                    if (!g[j]) continue;
+                    const uint32_t *e = reinterpret_cast<const uint32_t *>(&x[j]);
+                    const int v0 = (w0 * G::kVecsPerWord + j * kWave + lane) * G::kPerVec;
+#pragma unroll
+                    for (int k = 0; k < G::kPerVec; k++) {
+                        if (!((g[j] >> k) & 1)) continue;
+                        const uint32_t f = kBf16 ? ((k & 1) ? (e[k / 2] & 0xFFFF0000u) : (e[k / 2] << 16)) : e[k];
+                        const unsigned long long key = arg_key(f, v0 + k);
+                        best = key > best ? key : best;
+                    }
+                }
+            }
+        } else {
+            for (int v = threadIdx.x; v < V; v += kArgBlock) {
+                if (!((mrow[v >> 5] >> (v & 31)) & 1u)) continue;
+                const size_t idx = (size_t)b * V + v;
+                const uint32_t f = kBf16 ? (uint32_t)reinterpret_cast<const uint16_t *>(logits)[idx] << 16
+                                         : reinterpret_cast<const uint32_t *>(logits)[idx];
+                const unsigned long long key = arg_key(f, v);
+                best = key > best ? key : best;
+            }
+        }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const unsigned long long other = __shfl_xor(best, o, kWave);
+        best = other > best ? other : best;
+    }
+    if (lane == 0) s_best[wave] = best;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < kArgBlock / kWave; k++) best = s_best[k] > best ? s_best[k] : best;
+        out[b] = best ? (int32_t)(0xFFFFFFFFu - (uint32_t)best) : -1;
+    }
+}
+
 // ---------------------------------------------------------------- advance
 
 // The problem instance on the device (the lexing and parsing steps of
@@ -611,6 +701,44 @@ psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stri
     return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }
 
+// The masked argmax for ragged (stride 0) or strided stacks.
+psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
+                         const int32_t *lexer_states, int32_t B, const void *logits, psc_dtype dtype, int32_t V,
+                         int32_t *out_tokens, void *stream, const char *what) {
+    if (psc_status st = check_bound(h, what)) return st;
+    if (B < 0 || stride < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
+        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits || !out_tokens))) {
+        set_error(std::string(what) + ": null argument, negative size or bad dtype");
+        return PSC_E_INVALID_ARG;
+    }
+    if (V != h->V) {
+        set_error(std::string(what) + ": V differs from the vocabulary size");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B > 65535) {
+        set_error(std::string(what) + ": B > 65535");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(h->dev_base);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
+    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const int fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    dim3 grid(1, B);
+    if (dtype == PSC_BF16)
+        hipLaunchKernelGGL(argmax_kernel<true>, grid, dim3(kArgBlock), 0, s, table, masks, h->mask_stride, h->n_lex,
+                           h->n_lr, stacks, stride, stack_lens, lexer_states, V, h->W, err, logits, fast,
+                           out_tokens);
+    else
+        hipLaunchKernelGGL(argmax_kernel<false>, grid, dim3(kArgBlock), 0, s, table, masks, h->mask_stride,
+                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, h->W, err, logits,
+                           fast, out_tokens);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+}
+
 psc_status check_dense(const int32_t *stacks, int32_t cap, const int32_t *lens, const int32_t *qs, int32_t B,
                        const char *what) {
     if (B < 0 || cap < 1 || (B > 0 && (!stacks || !lens || !qs))) {
@@ -693,6 +821,23 @@ extern "C" psc_status psc_compute_and_apply_dense(const psc_handle *h, const int
         return st;
     return launch_fused(h, stacks, cap, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
                         "psc_compute_and_apply_dense");
+}
+
+extern "C" psc_status psc_compute_and_argmax(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                             const int32_t *lexer_states, int32_t B, const void *logits,
+                                             psc_dtype dtype, int32_t V, int32_t *out_tokens, void *stream) {
+    return launch_argmax(h, stacks, 0, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
+                         "psc_compute_and_argmax");
+}
+
+extern "C" psc_status psc_compute_and_argmax_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                                   const int32_t *stack_lens, const int32_t *lexer_states,
+                                                   int32_t B, const void *logits, psc_dtype dtype, int32_t V,
+                                                   int32_t *out_tokens, void *stream) {
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_and_argmax_dense"))
+        return st;
+    return launch_argmax(h, stacks, cap, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
+                         "psc_compute_and_argmax_dense");
 }
 
 extern "C" psc_status psc_state_reset(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,

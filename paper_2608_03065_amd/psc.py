@@ -21,8 +21,8 @@ _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E
 
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
             "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
-            "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_save", "psc_load",
-            "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_compute_and_argmax",
+            "psc_compute_and_argmax_dense", "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -81,6 +81,8 @@ def lib() -> C.CDLL:
         L.psc_compute_masks.argtypes = [P, P, P, P, I32, P, P]
         L.psc_apply_mask.argtypes = [P, C.c_int, P, I32, I32, P]
         L.psc_compute_and_apply.argtypes = [P, P, P, P, I32, P, P, C.c_int, I32, P]
+        L.psc_compute_and_argmax.argtypes = [P, P, P, P, I32, P, C.c_int, I32, P, P]
+        L.psc_compute_and_argmax_dense.argtypes = [P, P, I32, P, P, I32, P, C.c_int, I32, P, P]
         L.psc_save.argtypes = [P, C.c_char_p]
         L.psc_load.argtypes = [C.c_char_p, C.POINTER(P)]
         L.psc_state_reset.argtypes = [P, P, I32, P, P, I32, P]
@@ -95,7 +97,8 @@ def lib() -> C.CDLL:
         L.psc_last_error.restype = C.c_char_p
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
-                     "psc_compute_and_apply_dense", "psc_save", "psc_load", "psc_device_error_count",
+                     "psc_compute_and_apply_dense", "psc_compute_and_argmax", "psc_compute_and_argmax_dense",
+                     "psc_save", "psc_load", "psc_device_error_count",
                      "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -250,6 +253,23 @@ class Classifier:
                                            self.V, _stream_ptr(stream)))
         return logits
 
+    def compute_and_argmax(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
+        """Greedy token per sequence under its mask (int32 [B]; -1 = none
+        allowed); the logits are only read."""
+        import torch
+        B = int(stack_lens.shape[0])
+        for t in (stacks, stack_lens, lexer_states):
+            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
+        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (B, self.V)
+        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        if out is None:
+            out = torch.empty(B, dtype=torch.int32, device=logits.device)
+        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and out.numel() == B
+        _check(lib().psc_compute_and_argmax(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
+                                            lexer_states.data_ptr(), B, logits.data_ptr(), dt, self.V,
+                                            out.data_ptr(), _stream_ptr(stream)))
+        return out
+
     def error_count(self, reset: bool = False, stream=None) -> int:
         v = C.c_uint32()
         _check(lib().psc_device_error_count(self._h, C.byref(v), int(reset), _stream_ptr(stream)))
@@ -319,6 +339,19 @@ class DecodeStates:
                                                  self.lens.data_ptr(), self.qs.data_ptr(), self.B, out_ptr,
                                                  logits.data_ptr(), dt, self.clf.V, _stream_ptr(stream)))
         return logits
+
+    def argmax(self, logits, out=None, stream=None):
+        """Greedy token per sequence under its mask (int32 [B]; -1 = none)."""
+        import torch
+        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
+        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        if out is None:
+            out = torch.empty(self.B, dtype=torch.int32, device=logits.device)
+        _check(lib().psc_compute_and_argmax_dense(self.clf._h, self.stacks.data_ptr(), self.cap,
+                                                  self.lens.data_ptr(), self.qs.data_ptr(), self.B,
+                                                  logits.data_ptr(), dt, self.clf.V, out.data_ptr(),
+                                                  _stream_ptr(stream)))
+        return out
 
     def host_states(self):
         """The states as host (q, stack) pairs (synchronises)."""
