@@ -163,6 +163,15 @@ def main():
         t_apply = loop(only_apply, 1000)     # masks of steps 0..n_bm-1, as counted below
         t_compute = loop(only_compute, 1000)
 
+        # greedy decoding folded into the mask step (reads the logits only)
+        tok_out = torch.empty(B, dtype=torch.int32, device=dev)
+
+        def argmax_step(i):
+            stacks, lens, qs = step_inputs[i % n_distinct]
+            clf.compute_and_argmax(stacks, lens, qs, pool[i % n_pool], out=tok_out, stream=stream)
+
+        t_argmax = loop(argmax_step, 1000)
+
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
         # advanced by one token each (psc_advance), then the single-launch
         # step on them (psc_compute_and_apply_dense)
@@ -256,6 +265,7 @@ def main():
         "step_mode": args.mode,
         "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
         "decode_step_us": decode,
+        "argmax_step_us": round(t_argmax, 3),
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
                        "apply_mask_solo_gbs": round(achieved_apply, 1)},
         "bytes_per_step": {"algorithmic": round(bytes_step), "fused": round(bytes_fused),

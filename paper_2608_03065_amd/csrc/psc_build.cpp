@@ -917,7 +917,7 @@ using namespace psc;
 size_t psc_handle::device_bytes_needed() const {
     auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
     return kTableOff + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
-           up(gram.size() * sizeof(int32_t)) + vbytes.size();
+           up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes;
 }
 
 namespace {

@@ -393,9 +393,13 @@ fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restri
 // Greedy decoding folded into the mask step: out[b] = the allowed token with
 // the largest logit (ties to the lowest id; NaN above everything; -1 if no
 // token is allowed).  The logits are only read, and only the 16-byte vectors
-// holding at least one allowed token.  One workgroup per sequence walks once
-// and sweeps its whole row, so no reduction crosses workgroups.
-constexpr int kArgBlock = 1024;
+// holding at least one allowed token.  Two launches: argmax_partial_kernel
+// has the fused step's workgroups (one per sequence and slice of the row);
+// each folds its best (value, id) key into the sequence's slot with a 64-bit
+// atomic max, and argmax_finish_kernel, ordered after it by the launch
+// boundary, turns every slot into a token and clears it for the next call.
+// (A single launch would need device-scope fences between the workgroups of
+// a sequence, and those write back a whole L2 on this GPU.)
 
 // An order-preserving key: larger float, larger key; NaN above +inf; -0 = +0.
 __device__ __forceinline__ uint32_t order_key(uint32_t u) {
@@ -408,15 +412,19 @@ __device__ __forceinline__ unsigned long long arg_key(uint32_t fbits, int v) {
     return ((unsigned long long)order_key(fbits) << 32) | (0xFFFFFFFFu - (uint32_t)v);
 }
 
+__device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsigned long long b) {
+    return a > b ? a : b;
+}
+
 template <bool kBf16>
-__global__ void __launch_bounds__(kArgBlock)
-argmax_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-              int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
-              const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
-              uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
-              int32_t *__restrict__ out) {
+__global__ void __launch_bounds__(kBlock)
+argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                      int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
+                      const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
+                      uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
+                      unsigned long long *__restrict__ slots) {
     using G = ApplyGeom<kBf16>;
-    __shared__ unsigned long long s_best[kArgBlock / kWave];
+    __shared__ unsigned long long s_best[kBlock / kWave];
     const int b = blockIdx.y;
     const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -424,11 +432,12 @@ argmax_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ ma
     if (cls >= 0) {
         const uint32_t *mrow = masks + (size_t)cls * mask_stride;
         if (fast) {
-            // the apply's layout: a wavefront takes kWordsPerWave words, lane j
+            // the apply's layout: the wavefront's kWordsPerWave words, lane j
             // the vectors j, j + 64, ...; only vectors with an allowed token are read
-            const uint4 *row = reinterpret_cast<const uint4 *>(logits) + (size_t)b * W * G::kVecsPerWord;
             constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
-            for (int w0 = wave * G::kWordsPerWave; w0 < W; w0 += (kArgBlock / kWave) * G::kWordsPerWave) {
+            const int w0 = (blockIdx.x * (kBlock / kWave) + wave) * G::kWordsPerWave;
+            if (w0 < W) {
+                const uint4 *row = reinterpret_cast<const uint4 *>(logits) + ((size_t)b * W + w0) * G::kVecsPerWord;
                 const uint32_t m = lane < G::kWordsPerWave && w0 + lane < W ? mrow[w0 + lane] : 0u;
                 uint32_t g[G::kVecs];
                 uint4 x[G::kVecs];
@@ -439,7 +448,7 @@ argmax_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ ma
                 }
 #pragma unroll
                 for (int j = 0; j < G::kVecs; j++)
-                    if (g[j]) x[j] = load_nt(row + (size_t)w0 * G::kVecsPerWord + j * kWave + lane);
+                    if (g[j]) x[j] = load_nt(row + j * kWave + lane);
 #pragma unroll
                 for (int j = 0; j < G::kVecs; j++) {
                     if (!g[j]) continue;
@@ -449,33 +458,38 @@ argmax_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ ma
                     for (int k = 0; k < G::kPerVec; k++) {
                         if (!((g[j] >> k) & 1)) continue;
                         const uint32_t f = kBf16 ? ((k & 1) ? (e[k / 2] & 0xFFFF0000u) : (e[k / 2] << 16)) : e[k];
-                        const unsigned long long key = arg_key(f, v0 + k);
-                        best = key > best ? key : best;
+                        best = umax64(best, arg_key(f, v0 + k));
                     }
                 }
             }
         } else {
-            for (int v = threadIdx.x; v < V; v += kArgBlock) {
+            const int v_end = min(V, (blockIdx.x + 1) * kGenWords * 32);
+            for (int v = blockIdx.x * kGenWords * 32 + threadIdx.x; v < v_end; v += kBlock) {
                 if (!((mrow[v >> 5] >> (v & 31)) & 1u)) continue;
                 const size_t idx = (size_t)b * V + v;
                 const uint32_t f = kBf16 ? (uint32_t)reinterpret_cast<const uint16_t *>(logits)[idx] << 16
                                          : reinterpret_cast<const uint32_t *>(logits)[idx];
-                const unsigned long long key = arg_key(f, v);
-                best = key > best ? key : best;
+                best = umax64(best, arg_key(f, v));
             }
         }
     }
 #pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        const unsigned long long other = __shfl_xor(best, o, kWave);
-        best = other > best ? other : best;
-    }
+    for (int o = kWave / 2; o > 0; o >>= 1) best = umax64(best, __shfl_xor(best, o, kWave));
     if (lane == 0) s_best[wave] = best;
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int k = 1; k < kArgBlock / kWave; k++) best = s_best[k] > best ? s_best[k] : best;
-        out[b] = best ? (int32_t)(0xFFFFFFFFu - (uint32_t)best) : -1;
+        for (int k = 1; k < kBlock / kWave; k++) best = umax64(best, s_best[k]);
+        if (best) atomicMax(slots + b, best);
     }
+}
+
+__global__ void __launch_bounds__(kBlock)
+argmax_finish_kernel(unsigned long long *__restrict__ slots, int32_t B, int32_t *__restrict__ out) {
+    const int b = blockIdx.x * kBlock + threadIdx.x;
+    if (b >= B) return;
+    const unsigned long long k = slots[b];
+    slots[b] = 0;
+    out[b] = k ? (int32_t)(0xFFFFFFFFu - (uint32_t)k) : -1;
 }
 
 // ---------------------------------------------------------------- advance
@@ -726,15 +740,24 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
     const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
     uint32_t *err = reinterpret_cast<uint32_t *>(base);
     const int fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
-    dim3 grid(1, B);
+    const int32_t W = h->W;
+    const int words_per_block = !fast ? kGenWords
+                                      : (kBlock / kWave) * (dtype == PSC_BF16 ? ApplyGeom<true>::kWordsPerWave
+                                                                              : ApplyGeom<false>::kWordsPerWave);
+    dim3 grid((W + words_per_block - 1) / words_per_block, B);
+    auto *slots = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
     if (dtype == PSC_BF16)
-        hipLaunchKernelGGL(argmax_kernel<true>, grid, dim3(kArgBlock), 0, s, table, masks, h->mask_stride, h->n_lex,
-                           h->n_lr, stacks, stride, stack_lens, lexer_states, V, h->W, err, logits, fast,
-                           out_tokens);
+        hipLaunchKernelGGL(argmax_partial_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
+                           slots);
     else
-        hipLaunchKernelGGL(argmax_kernel<false>, grid, dim3(kArgBlock), 0, s, table, masks, h->mask_stride,
-                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, h->W, err, logits,
-                           fast, out_tokens);
+        hipLaunchKernelGGL(argmax_partial_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
+                           slots);
+    hipError_t e0 = hipGetLastError();
+    if (e0 != hipSuccess) return device_fail(what, e0);
+    hipLaunchKernelGGL(argmax_finish_kernel, dim3((B + kBlock - 1) / kBlock), dim3(kBlock), 0, s, slots, B,
+                       out_tokens);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }
@@ -770,7 +793,9 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     const size_t mask_off = kTableOff + up(h->table.size() * sizeof(int32_t));
     const size_t gram_off = mask_off + up(h->masks.size() * sizeof(uint32_t));
     const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
+    const size_t argmax_off = vbytes_off + up(h->vbytes.size());
     hipError_t e = hipMemsetAsync(base, 0, kTableOff, s);
+    if (e == hipSuccess) e = hipMemsetAsync(base + argmax_off, 0, kArgmaxBytes, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + kTableOff, h->table.data(), h->table.size() * sizeof(int32_t),
                            hipMemcpyHostToDevice, s);
@@ -789,6 +814,7 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     h->mask_off = mask_off;
     h->gram_off = gram_off;
     h->vbytes_off = vbytes_off;
+    h->argmax_off = argmax_off;
     return PSC_OK;
 }
 

@@ -71,7 +71,9 @@ struct AdvanceLayout {
 //   [mask_off, ...)            uint32 masks [n_classes][mask_stride] (256-B aligned)
 //   [gram_off, ...)            int32 advance blob (AdvanceLayout)
 //   [vbytes_off, ...)          uint8 vocabulary bytes
+//   [argmax_off, ...)          uint64 [65536] masked-argmax slots (zero between calls)
 constexpr size_t kTableOff = 256;
+constexpr size_t kArgmaxBytes = 65536 * sizeof(unsigned long long);
 
 }  // namespace psc
 
@@ -87,7 +89,7 @@ struct psc_handle {
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
-    size_t mask_off = 0, gram_off = 0, vbytes_off = 0;
+    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0;
     size_t device_bytes_needed() const;
 };
 

@@ -91,6 +91,7 @@ def test_argmax_rejected_rows(built):
     states = [good, (wl.grammar.lexer.n_states, good[1]), good]
     stacks, lens, qs = pack_states(states, DEV)
     logits = torch.randn(3, wl.V, device=DEV)
+    logits[2] = logits[0]                      # same state, same logits: same token
     got = clf.compute_and_argmax(stacks, lens, qs, logits).cpu().numpy()
     assert got[1] == -1 and got[0] == got[2] and got[0] >= 0
     assert clf.error_count(reset=True) == 1
