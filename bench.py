@@ -172,6 +172,25 @@ def main():
 
         t_argmax = loop(argmax_step, 1000)
 
+        # the timed step captured in a HIP graph: G steps (rotating inputs
+        # and logits as above) per graph, replayed back to back
+        G = 100
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for i in range(G):
+                step(i)
+        graph.replay()
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        reps = max(1, min(args.steps, 2000) // G)
+        for _ in range(reps):
+            graph.replay()
+        z.record(stream)
+        torch.cuda.synchronize()
+        t_graph = a.elapsed_time(z) / (reps * G) * 1e3
+        del graph
+
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
         # advanced by one token each (psc_advance), then the single-launch
         # step on them (psc_compute_and_apply_dense)
@@ -266,6 +285,7 @@ def main():
         "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
         "decode_step_us": decode,
         "argmax_step_us": round(t_argmax, 3),
+        "graph_step_us": round(t_graph, 3),
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
                        "apply_mask_solo_gbs": round(achieved_apply, 1)},
         "bytes_per_step": {"algorithmic": round(bytes_step), "fused": round(bytes_fused),
