@@ -330,13 +330,19 @@ apply_generic_kernel(void *__restrict__ logits, const uint32_t *__restrict__ bit
 // ---------------------------------------------------------------- fused step
 
 // psc_compute_and_apply, fast path (V % 32 == 0, 16-byte aligned logits):
-// one workgroup per (sequence b, slice of kBlock / kWave * kWordsPerWave mask
-// words).  After the walk, every wavefront loads its words of the class's
-// mask row once, writes them to out_bitmask[b] (when requested) and applies
-// them to logits[b] in place.  One launch instead of two, and the bitmask is
-// not read back from HBM between the gather and the apply.
+// one workgroup per (sequence b, slice of kFusedBlock / kWave *
+// kWordsPerWave mask words).  After the walk, every wavefront loads its words
+// of the class's mask row once, writes them to out_bitmask[b] (when
+// requested) and applies them to logits[b] in place.  One launch instead of
+// two, and the bitmask is not read back from HBM between the gather and the
+// apply.  Four wavefronts per workgroup (2 measured slightly faster on a
+// 200-step schema sample but slower over the 1,000-step schema workload and
+// on the largest one); the walk is repeated per workgroup, which costs
+// latency but no bandwidth.
+constexpr int kFusedBlock = 4 * kWave;
+
 template <bool kBf16>
-__global__ void __launch_bounds__(kBlock)
+__global__ void __launch_bounds__(kFusedBlock)
 fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
                   int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
                   const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
@@ -345,7 +351,7 @@ fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict_
     const int b = blockIdx.y;
     const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1);
-    const int w_base = (blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * G::kWordsPerWave;
+    const int w_base = (blockIdx.x * (kFusedBlock / kWave) + threadIdx.x / kWave) * G::kWordsPerWave;
     if (w_base >= W) return;
     uint32_t m = 0xFFFFFFFFu;
     const int w = w_base + lane;
@@ -417,14 +423,14 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsig
 }
 
 template <bool kBf16>
-__global__ void __launch_bounds__(kBlock)
+__global__ void __launch_bounds__(kFusedBlock)
 argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
                       int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
                       const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
                       uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
                       unsigned long long *__restrict__ slots) {
     using G = ApplyGeom<kBf16>;
-    __shared__ unsigned long long s_best[kBlock / kWave];
+    __shared__ unsigned long long s_best[kFusedBlock / kWave];
     const int b = blockIdx.y;
     const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -435,7 +441,7 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
             // the apply's layout: the wavefront's kWordsPerWave words, lane j
             // the vectors j, j + 64, ...; only vectors with an allowed token are read
             constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
-            const int w0 = (blockIdx.x * (kBlock / kWave) + wave) * G::kWordsPerWave;
+            const int w0 = (blockIdx.x * (kFusedBlock / kWave) + wave) * G::kWordsPerWave;
             if (w0 < W) {
                 const uint4 *row = reinterpret_cast<const uint4 *>(logits) + ((size_t)b * W + w0) * G::kVecsPerWord;
                 const uint32_t m = lane < G::kWordsPerWave && w0 + lane < W ? mrow[w0 + lane] : 0u;
@@ -464,7 +470,7 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
             }
         } else {
             const int v_end = min(V, (blockIdx.x + 1) * kGenWords * 32);
-            for (int v = blockIdx.x * kGenWords * 32 + threadIdx.x; v < v_end; v += kBlock) {
+            for (int v = blockIdx.x * kGenWords * 32 + threadIdx.x; v < v_end; v += kFusedBlock) {
                 if (!((mrow[v >> 5] >> (v & 31)) & 1u)) continue;
                 const size_t idx = (size_t)b * V + v;
                 const uint32_t f = kBf16 ? (uint32_t)reinterpret_cast<const uint16_t *>(logits)[idx] << 16
@@ -478,7 +484,7 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
     if (lane == 0) s_best[wave] = best;
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int k = 1; k < kBlock / kWave; k++) best = umax64(best, s_best[k]);
+        for (int k = 1; k < kFusedBlock / kWave; k++) best = umax64(best, s_best[k]);
         if (best) atomicMax(slots + b, best);
     }
 }
@@ -689,15 +695,15 @@ psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stri
     const bool bf16 = dtype == PSC_BF16;
     const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
     if (fast) {
-        const int words_per_block = (kBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
-                                                             : ApplyGeom<false>::kWordsPerWave);
+        const int words_per_block = (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
+                                                                  : ApplyGeom<false>::kWordsPerWave);
         dim3 grid((W + words_per_block - 1) / words_per_block, B);
         if (bf16)
-            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                                h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
                                reinterpret_cast<uint4 *>(logits));
         else
-            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                                h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
                                reinterpret_cast<uint4 *>(logits));
     } else {
@@ -742,16 +748,16 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
     const int fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
     const int32_t W = h->W;
     const int words_per_block = !fast ? kGenWords
-                                      : (kBlock / kWave) * (dtype == PSC_BF16 ? ApplyGeom<true>::kWordsPerWave
-                                                                              : ApplyGeom<false>::kWordsPerWave);
+                                      : (kFusedBlock / kWave) * (dtype == PSC_BF16 ? ApplyGeom<true>::kWordsPerWave
+                                                                                   : ApplyGeom<false>::kWordsPerWave);
     dim3 grid((W + words_per_block - 1) / words_per_block, B);
     auto *slots = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
     if (dtype == PSC_BF16)
-        hipLaunchKernelGGL(argmax_partial_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+        hipLaunchKernelGGL(argmax_partial_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                            h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
                            slots);
     else
-        hipLaunchKernelGGL(argmax_partial_kernel<false>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
+        hipLaunchKernelGGL(argmax_partial_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                            h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
                            slots);
     hipError_t e0 = hipGetLastError();
