@@ -39,6 +39,18 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
     return make_uint4(x.x, x.y, x.z, x.w);
 }
 
+// A raw buffer resource (no stride, no swizzle, 32-bit data format: the
+// gfx9-family encoding of the descriptor's last word) over `bytes` bytes at
+// p.  Accesses at a byte offset >= bytes are out of range: the hardware
+// drops them, and a load returns zeros.
+constexpr int32_t kRsrcWord3 = 0x00020000;
+constexpr uint32_t kOffSkip = 0x80000000u;   // an offset past any resource used here
+constexpr int kPolicyNt = 2;                  // cache policy: nontemporal (streaming)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int32_t)bytes, kRsrcWord3);
+}
+
 // Walk of sequence b by one wavefront (Algorithm 2, classification step):
 // ref = start[q]; read the stack top-first; stop as soon as ref names a
 // class (a determined state).  The walk is a chain of dependent loads, so
@@ -225,9 +237,22 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
     const uint32_t *src = masks + (size_t)cls * mask_stride;
     if (vec4) {
         // W % 4 == 0 and out is 16-byte aligned: 128-bit loads and stores
+        // every load is issued before the first store, so no store waits
+        // for another to complete
         const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
         uint4 *d4 = reinterpret_cast<uint4 *>(dst);
-        for (int w = w0 / 4 + tid; w < w1 / 4; w += kBlock) store_nt(d4 + w, load_nt(s4 + w));
+        constexpr int kPer = kCopyWordsPerBlock / 4 / kBlock;
+        uint4 v[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; k++) {
+            const int w = w0 / 4 + tid + k * kBlock;
+            if (w < w1 / 4) v[k] = load_nt(s4 + w);
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; k++) {
+            const int w = w0 / 4 + tid + k * kBlock;
+            if (w < w1 / 4) store_nt(d4 + w, v[k]);
+        }
     } else {
         for (int w = w0 + tid; w < w1; w += kBlock) dst[w] = src[w];
     }
@@ -256,12 +281,22 @@ struct ApplyGeom {
     static constexpr int kWordsPerWave = kWave * kVecs / kVecsPerWord;
 };
 
+//
+// The loads and stores go through a buffer resource over the wavefront's
+// `bytes` bytes of logits.  A lane that must not touch its vector gets an
+// offset past the end instead of a branch: the hardware drops such an access
+// (a load returns zeros) without a memory request.  Every memory instruction
+// is then issued unconditionally, so the compiler counts them exactly: the
+// selects wait for their loads only, and no store waits for an earlier
+// store to complete (with branches it had to wait for all outstanding
+// accesses before each vector, which serialised the stores).
 template <bool kBf16>
-__device__ __forceinline__ void apply_words(uint4 *__restrict__ base, uint32_t m, int lane) {
+__device__ __forceinline__ void apply_words(uint4 *__restrict__ base, uint32_t bytes, uint32_t m, int lane) {
     using G = ApplyGeom<kBf16>;
     constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
+    const __amdgpu_buffer_rsrc_t rsrc = wave_rsrc(base, bytes);
     uint32_t g[G::kVecs];
-    uint4 x[G::kVecs];
+    u32x4 x[G::kVecs];
 #pragma unroll
     for (int j = 0; j < G::kVecs; j++) {
         // vector v = j*64 + lane covers elements [kPerVec*v, kPerVec*v + kPerVec)
@@ -269,32 +304,28 @@ __device__ __forceinline__ void apply_words(uint4 *__restrict__ base, uint32_t m
         g[j] = (__shfl(m, v / G::kVecsPerWord, kWave) >> ((v % G::kVecsPerWord) * G::kPerVec)) & kFull;
     }
 #pragma unroll
-    for (int j = 0; j < G::kVecs; j++)
-        if (g[j] != 0 && g[j] != kFull) x[j] = load_nt(base + j * kWave + lane);
+    for (int j = 0; j < G::kVecs; j++) {
+        const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
+        x[j] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, g[j] != 0 && g[j] != kFull ? off : kOffSkip, 0,
+                                                     kPolicyNt);
+    }
 #pragma unroll
     for (int j = 0; j < G::kVecs; j++) {
-        if (g[j] == kFull) continue;
-        uint4 val;
-        if (g[j] == 0) {
-            const uint32_t ni = kBf16 ? (((uint32_t)kBf16NegInf << 16) | kBf16NegInf) : kF32NegInf;
-            val = make_uint4(ni, ni, ni, ni);
-        } else {
-            val = x[j];
-            uint32_t *e = reinterpret_cast<uint32_t *>(&val);
-            if (kBf16) {
+        u32x4 val = x[j];
+        if (kBf16) {
 #pragma unroll
-                for (int k = 0; k < 4; k++) {
-                    const uint32_t lo = (g[j] >> (2 * k)) & 1 ? (e[k] & 0xFFFFu) : kBf16NegInf;
-                    const uint32_t hi = (g[j] >> (2 * k + 1)) & 1 ? (e[k] >> 16) : kBf16NegInf;
-                    e[k] = lo | (hi << 16);
-                }
-            } else {
-#pragma unroll
-                for (int k = 0; k < 4; k++)
-                    if (!((g[j] >> k) & 1)) e[k] = kF32NegInf;
+            for (int k = 0; k < 4; k++) {
+                const uint32_t lo = (g[j] >> (2 * k)) & 1 ? (val[k] & 0xFFFFu) : kBf16NegInf;
+                const uint32_t hi = (g[j] >> (2 * k + 1)) & 1 ? (val[k] >> 16) : kBf16NegInf;
+                val[k] = lo | (hi << 16);
             }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; k++)
+                if (!((g[j] >> k) & 1)) val[k] = kF32NegInf;
         }
-        store_nt(base + j * kWave + lane, val);
+        const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
+        __builtin_amdgcn_raw_buffer_store_b128(val, rsrc, g[j] != kFull ? off : kOffSkip, 0, kPolicyNt);
     }
 }
 
@@ -305,12 +336,16 @@ __global__ void __launch_bounds__(kBlock)
 apply_fast_kernel(uint4 *__restrict__ logits, const uint32_t *__restrict__ bits, int64_t n_words) {
     using G = ApplyGeom<kBf16>;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    // the wavefront index is uniform: saying so keeps the buffer resource in
+    // scalar registers
+    const int64_t wave = (int64_t)blockIdx.x * (kBlock / kWave) +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t w_base = wave * G::kWordsPerWave;
     if (w_base >= n_words) return;
     uint32_t m = 0xFFFFFFFFu;
     if (lane < G::kWordsPerWave && w_base + lane < n_words) m = bits[w_base + lane];
-    apply_words<kBf16>(logits + w_base * G::kVecsPerWord, m, lane);
+    const uint32_t words = (uint32_t)min<int64_t>(G::kWordsPerWave, n_words - w_base);
+    apply_words<kBf16>(logits + w_base * G::kVecsPerWord, words * G::kVecsPerWord * 16u, m, lane);
 }
 
 // General path: any V and alignment, one element per thread.
@@ -351,15 +386,18 @@ fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict_
     const int b = blockIdx.y;
     const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1);
-    const int w_base = (blockIdx.x * (kFusedBlock / kWave) + threadIdx.x / kWave) * G::kWordsPerWave;
+    const int w_base =
+        (blockIdx.x * (kFusedBlock / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave)) * G::kWordsPerWave;
     if (w_base >= W) return;
     uint32_t m = 0xFFFFFFFFu;
     const int w = w_base + lane;
-    if (lane < G::kWordsPerWave && w < W) {
-        m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w];
-        if (out) out[(size_t)b * W + w] = m;
-    }
-    apply_words<kBf16>(logits + ((size_t)b * W + w_base) * G::kVecsPerWord, m, lane);
+    const bool mine = lane < G::kWordsPerWave && w < W;
+    if (mine) m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w];
+    const uint32_t words = (uint32_t)min(G::kWordsPerWave, W - w_base);
+    apply_words<kBf16>(logits + ((size_t)b * W + w_base) * G::kVecsPerWord, words * G::kVecsPerWord * 16u, m,
+                       lane);
+    // last, so that the logits accesses never wait for this store
+    if (out && mine) out[(size_t)b * W + w] = m;
 }
 
 // psc_compute_and_apply, general path (any V, any element alignment): one
