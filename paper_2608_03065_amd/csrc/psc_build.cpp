@@ -1149,6 +1149,21 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
                 chains.push_back(std::move(ch));
             }
         }
+        // A chain shorter than kChainReach goes on with copies of the thin
+        // states that follow its last one, so that a walk crossing into the
+        // next chain does not pay a load for the jump between them; copies
+        // are entries like the originals, but no ref points at them.
+        std::vector<std::vector<int32_t>> laid(chains.size());
+        std::vector<int32_t> jump_to(chains.size());
+        for (size_t c = 0; c < chains.size(); c++) {
+            laid[c] = chains[c];
+            int32_t t = cont_target(chains[c].back());
+            while ((int)laid[c].size() < kChainReach && is_thin(t)) {
+                laid[c].push_back(t);
+                t = cont_target(t);
+            }
+            jump_to[c] = t;
+        }
         int64_t off = (G.nQ + 3) & ~3;
         h->rows_off = off;
         int32_t rows = 0, dense = 0, max_sparse = 0, chain_states = 0;
@@ -1165,9 +1180,10 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
         }
         h->chains_off = off;
-        for (const auto &ch : chains) {
+        for (size_t c = 0; c < chains.size(); c++) {
+            const auto &ch = chains[c];
             for (size_t j = 0; j < ch.size(); j++) ref[ch[j]] = (int32_t)(off + kChainEntry * j) | kRefChain;
-            off += kChainEntry * (int64_t)(ch.size() + 1);
+            off += kChainEntry * (int64_t)(laid[c].size() + 1);
             chain_states += (int32_t)ch.size();
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
         }
@@ -1193,9 +1209,9 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
                 }
             }
         }
-        for (const auto &ch : chains) {
-            int32_t *e = h->table.data() + ref_offset(ref[ch[0]]);
-            for (int32_t b : ch) {
+        for (size_t c = 0; c < chains.size(); c++) {
+            int32_t *e = h->table.data() + ref_offset(ref[chains[c][0]]);
+            for (int32_t b : laid[c]) {
                 const int32_t ce = cont_edge(b);
                 uint32_t a = ce < 0 ? (uint32_t)kSymWild : (uint32_t)m_sym[ce], bs = kSymNone;
                 int32_t rb = 0;
@@ -1209,7 +1225,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             }
             e[0] = (int32_t)((uint32_t)kSymJump | ((uint32_t)kSymNone << 16));
             e[1] = 0;
-            e[2] = ref[cont_target(ch.back())];
+            e[2] = ref[jump_to[c]];
             e[3] = 0;
         }
         h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);

@@ -964,7 +964,7 @@ extern "C" psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32
     const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
     if (fast) {
         const int64_t n_words = (int64_t)B * W;
-        const int64_t words_per_wave = bf16 ? 64 : 32;           // 4 vectors per lane
+        const int64_t words_per_wave = bf16 ? ApplyGeom<true>::kWordsPerWave : ApplyGeom<false>::kWordsPerWave;
         const int64_t waves = (n_words + words_per_wave - 1) / words_per_wave;
         const int64_t blocks = (waves + (kBlock / kWave) - 1) / (kBlock / kWave);
         if (blocks > 0x7FFFFFFF) {

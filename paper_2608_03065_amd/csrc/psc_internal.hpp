@@ -32,11 +32,15 @@ namespace psc {
 //   chain continues with, reached without reading a symbol);  w = the
 //   state's end_class (the class when the stack ends before it reads).
 // A chain holds at most kChainMax states and ends with a kSymJump entry, so
-// 64 consecutive entries read from any state of it include that entry.
+// 64 consecutive entries read from any state of it include that entry.  A
+// chain of fewer than kChainReach states is followed, before its jump, by
+// copies of the thin states its last state continues into (their entries,
+// never pointed at by a ref), up to kChainReach entries in all.
 // Rows and entries start at multiples of 4 int32 (16-byte aligned).
 constexpr int kRowHeader = 4;
 constexpr int kSparseMax = 62;      // header + edges in one wavefront-wide load
 constexpr int kChainMax = 63;
+constexpr int kChainReach = 16;     // entries a chain is extended to with copies of its continuation
 constexpr int kChainEntry = 4;      // int32 per entry
 constexpr int32_t kSymNone = 0xFFFF, kSymWild = 0xFFFE, kSymJump = 0xFFFD;
 constexpr int kMaxChainAlphabet = 0xFFFD;   // chains need every symbol < kSymJump
