@@ -244,6 +244,12 @@ def main():
             "algorithmic_bytes_per_launch": round(bytes_fused),
             "avg_launch_us": round(lat_us, 3),
             "timing": "HIP events on the bench stream around the timed loop; one launch per step",
+            # the read-every-logit-and-write-it-back byte model, for comparison
+            # only: the kernel does not move these bytes (fully masked vectors
+            # are only written, kept ones not touched)
+            "one_pass_model": {"bytes": round(one_pass_model),
+                               "gbs": round(one_pass_model / (lat_us * 1e-6) / 1e9, 1),
+                               "frac": round(one_pass_model / (lat_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
         }
     else:
         kname = "apply_fast_kernel" if fast else "apply_generic_kernel"
