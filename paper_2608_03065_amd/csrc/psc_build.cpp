@@ -917,8 +917,28 @@ using namespace psc;
 size_t psc_handle::device_bytes_needed() const {
     auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
     return kTableOff + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
-           up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes;
+           up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes +
+           up((size_t)n_lr * adv.n_term * sizeof(int32_t));
 }
+
+namespace psc {
+bool packed_action(const psc_handle &h, std::vector<int32_t> &out) {
+    out.clear();
+    const AdvanceLayout &L = h.adv;
+    const int32_t *act = h.gram.data() + L.action, *lhs = h.gram.data() + L.prod_lhs,
+                  *len = h.gram.data() + L.prod_len;
+    const int64_t n = (int64_t)h.n_lr * L.n_term;
+    std::vector<int32_t> v(act, act + n);
+    for (int32_t &a : v) {
+        if ((a & 3) != 2) continue;
+        const int32_t p = a >> 2;
+        if (len[p] > 255 || lhs[p] >= (1 << 21)) return false;
+        a = 2 | (len[p] << 2) | (lhs[p] << 10);
+    }
+    out.swap(v);
+    return true;
+}
+}  // namespace psc
 
 namespace {
 // Keep the problem instance for the device advance (the lexing and parsing

@@ -544,62 +544,80 @@ struct AdvTables {
     const int32_t *lex_next, *lex_accept, *ignored, *action, *go, *prod_lhs, *prod_len, *tok_off;
     const uint8_t *bytes;
     int32_t n_lex, n_lr, n_term, n_nt, end_term, eos, V;
+    int32_t packed;    // action holds packed reductions (kind | len << 2 | lhs << 10)
 };
 
-constexpr int kAdvBlock = 64;          // sequences per workgroup (one per thread)
 constexpr int kOverlay = 192;          // states one token may push above what it keeps
 constexpr int kFeedSteps = 1 << 16;    // bound on the LR steps of one terminal
 
-// One thread advances one sequence by one token.  While the token is
-// processed the kept part of the stack, stacks[b][0 .. ptr), is only read and
-// the states pushed above it live in an LDS overlay, so a rejected token
+// One wavefront advances one sequence by one token.  Everything it computes
+// is uniform across the wavefront (the sequence is the workgroup's), so the
+// table reads are scalar loads with one address each, and no sequence waits
+// for another's path through the lexer and the parser.  The token's bytes
+// are fetched up front, 64 at a time, one per lane.  While the token is
+// processed the kept part of the stack, stacks[b][0 .. ptr), is only read
+// and the states pushed above it live in an LDS overlay, so a rejected token
 // leaves the stack, its length and the lexer state exactly as they were; on
 // success the overlay is written above ptr.  A terminal is fed as the LR
 // parser does: the reductions its lookahead selects, then a shift (accept
 // for $end); popping the whole stack or a missing goto rejects.
-__global__ void __launch_bounds__(kAdvBlock)
+__global__ void __launch_bounds__(kWave)
 advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ lens,
                int32_t *__restrict__ qs, int32_t B, const int32_t *__restrict__ tokens,
                int32_t *__restrict__ status) {
-    __shared__ int32_t s_ov[kOverlay][kAdvBlock];
-    const int b = blockIdx.x * kAdvBlock + threadIdx.x;
-    if (b >= B) return;
+    __shared__ int32_t s_ov[kOverlay];
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x;
     const int tok = tokens[b];
-    if (tok < 0) { status[b] = PSC_ADV_SKIPPED; return; }
+    if (tok < 0) {
+        if (lane == 0) status[b] = PSC_ADV_SKIPPED;
+        return;
+    }
     const int len = lens[b], q_in = qs[b];
     if (tok >= T.V || len < 1 || len > cap || q_in < 0 || q_in >= T.n_lex) {
-        status[b] = PSC_ADV_BAD_INPUT;
+        if (lane == 0) status[b] = PSC_ADV_BAD_INPUT;
         return;
     }
     const int32_t *st = stacks + (int64_t)b * cap;
     int ptr = len, ov = 0;
-    auto top = [&]() { return ov > 0 ? s_ov[ov - 1][threadIdx.x] : st[ptr - 1]; };
+    int32_t cur = st[ptr - 1];   // the top of the stack, kept in a register
+    auto reload = [&]() { cur = __builtin_amdgcn_readfirstlane(ov > 0 ? s_ov[ov - 1] : st[ptr - 1]); };
     auto push = [&](int32_t x) {
         if (ov >= kOverlay) return false;
-        s_ov[ov++][threadIdx.x] = x;
+        s_ov[ov++] = x;          // every lane writes the same value
+        cur = x;
         return true;
     };
     // states come from the tables (validated when built) or, below the
     // overlay, from the caller's stack, which is checked before each use
     auto feed = [&](int32_t t) -> int {
         for (int guard = 0; guard < kFeedSteps; guard++) {
-            const int32_t s0 = top();
+            const int32_t s0 = cur;
             if (s0 < 0 || s0 >= T.n_lr) return PSC_ADV_BAD_INPUT;
             const int32_t a = T.action[(int64_t)s0 * T.n_term + t];
             const int kind = a & 3;
             if (kind == 1) return push(a >> 2) ? PSC_ADV_OK : PSC_ADV_OVERFLOW;
             if (kind == 3) return PSC_ADV_OK;
             if (kind == 0) return PSC_ADV_REJECTED;
-            const int32_t p = a >> 2;
-            int k = T.prod_len[p];
+            int32_t lhs;
+            int k;
+            if (T.packed) {
+                lhs = a >> 10;
+                k = (a >> 2) & 255;
+            } else {
+                const int32_t p = a >> 2;
+                lhs = T.prod_lhs[p];
+                k = T.prod_len[p];
+            }
             const int from_ov = min(k, ov);
             ov -= from_ov;
             k -= from_ov;
             if (k >= ptr) return PSC_ADV_REJECTED;       // nothing left to goto from
             ptr -= k;
-            const int32_t s1 = top();
+            reload();
+            const int32_t s1 = cur;
             if (s1 < 0 || s1 >= T.n_lr) return PSC_ADV_BAD_INPUT;
-            const int32_t g = T.go[(int64_t)s1 * T.n_nt + T.prod_lhs[p]];
+            const int32_t g = T.go[(int64_t)s1 * T.n_nt + lhs];
             if (g < 0) return PSC_ADV_REJECTED;
             if (!push(g)) return PSC_ADV_OVERFLOW;
         }
@@ -621,32 +639,39 @@ advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *
             const int r = feed(T.end_term);
             if (r != PSC_ADV_OK) res = r;
         }
-        status[b] = res;
+        if (lane == 0) status[b] = res;
         return;
     }
     // longest match with one byte of lookahead: a byte the pending lexeme
     // cannot take ends it (it must be accepting) and starts the next from q0
-    for (int i = T.tok_off[tok], e = T.tok_off[tok + 1]; i < e; i++) {
-        const int c = T.bytes[i];
-        const int32_t nx = T.lex_next[(int64_t)q * 256 + c];
-        if (nx >= 0) { q = nx; continue; }
-        const int32_t t = q != 0 ? T.lex_accept[q] : -1;
-        if (t < 0) { res = PSC_ADV_REJECTED; break; }
-        if (!T.ignored[t]) {
-            res = feed(t);
-            if (res != PSC_ADV_OK) break;
+    const int i0 = T.tok_off[tok], n = T.tok_off[tok + 1] - i0;
+    for (int base = 0; base < n && res == PSC_ADV_OK; base += kWave) {
+        const int chunk = __builtin_amdgcn_readfirstlane(min(kWave, n - base));
+        const int byte = lane < chunk ? T.bytes[i0 + base + lane] : 0;
+        for (int j = 0; j < chunk; j++) {
+            const int c = __builtin_amdgcn_readlane(byte, j);
+            const int32_t nx = T.lex_next[(int64_t)q * 256 + c];
+            if (nx >= 0) { q = nx; continue; }
+            const int32_t t = q != 0 ? T.lex_accept[q] : -1;
+            if (t < 0) { res = PSC_ADV_REJECTED; break; }
+            if (!T.ignored[t]) {
+                res = feed(t);
+                if (res != PSC_ADV_OK) break;
+            }
+            q = T.lex_next[c];
+            if (q < 0) { res = PSC_ADV_REJECTED; break; }
         }
-        q = T.lex_next[c];
-        if (q < 0) { res = PSC_ADV_REJECTED; break; }
     }
     if (res == PSC_ADV_OK && ptr + ov > cap) res = PSC_ADV_OVERFLOW;
     if (res == PSC_ADV_OK) {
         int32_t *dst = stacks + (int64_t)b * cap + ptr;
-        for (int k = 0; k < ov; k++) dst[k] = s_ov[k][threadIdx.x];
-        lens[b] = ptr + ov;
-        qs[b] = q;
+        for (int k = lane; k < ov; k += kWave) dst[k] = s_ov[k];
+        if (lane == 0) {
+            lens[b] = ptr + ov;
+            qs[b] = q;
+        }
     }
-    status[b] = res;
+    if (lane == 0) status[b] = res;
 }
 
 // Every sequence back to the empty prefix: lexer state q0, stack [0].
@@ -838,6 +863,9 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     const size_t gram_off = mask_off + up(h->masks.size() * sizeof(uint32_t));
     const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
     const size_t argmax_off = vbytes_off + up(h->vbytes.size());
+    const size_t packed_off = argmax_off + kArgmaxBytes;
+    std::vector<int32_t> packed;
+    const bool is_packed = packed_action(*h, packed);
     hipError_t e = hipMemsetAsync(base, 0, kTableOff, s);
     if (e == hipSuccess) e = hipMemsetAsync(base + argmax_off, 0, kArgmaxBytes, s);
     if (e == hipSuccess)
@@ -851,6 +879,9 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
                            hipMemcpyHostToDevice, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + vbytes_off, h->vbytes.data(), h->vbytes.size(), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && is_packed)
+        e = hipMemcpyAsync(base + packed_off, packed.data(), packed.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                           s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return device_fail("psc_bind_device", e);
     h->dev_base = dev_buf;
@@ -859,6 +890,8 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     h->gram_off = gram_off;
     h->vbytes_off = vbytes_off;
     h->argmax_off = argmax_off;
+    h->packed_off = packed_off;
+    h->action_packed = is_packed;
     return PSC_OK;
 }
 
@@ -937,10 +970,11 @@ extern "C" psc_status psc_advance(const psc_handle *h, int32_t *stacks, int32_t 
     const char *base = static_cast<const char *>(h->dev_base);
     const int32_t *g = reinterpret_cast<const int32_t *>(base + h->gram_off);
     const psc::AdvanceLayout &L = h->adv;
-    AdvTables T{g + L.lex_next, g + L.lex_accept, g + L.ignored, g + L.action, g + L.go, g + L.prod_lhs,
+    const int32_t *action = h->action_packed ? reinterpret_cast<const int32_t *>(base + h->packed_off) : g + L.action;
+    AdvTables T{g + L.lex_next, g + L.lex_accept, g + L.ignored, action, g + L.go, g + L.prod_lhs,
                 g + L.prod_len, g + L.tok_off, reinterpret_cast<const uint8_t *>(base + h->vbytes_off),
-                h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V};
-    hipLaunchKernelGGL(advance_kernel, dim3((B + kAdvBlock - 1) / kAdvBlock), dim3(kAdvBlock), 0,
+                h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0};
+    hipLaunchKernelGGL(advance_kernel, dim3(B), dim3(kWave), 0,
                        reinterpret_cast<hipStream_t>(stream), T, stacks, cap, stack_lens, lexer_states, B, tokens,
                        status);
     hipError_t e = hipGetLastError();

@@ -76,6 +76,7 @@ struct AdvanceLayout {
 //   [gram_off, ...)            int32 advance blob (AdvanceLayout)
 //   [vbytes_off, ...)          uint8 vocabulary bytes
 //   [argmax_off, ...)          uint64 [65536] masked-argmax slots (zero between calls)
+//   [packed_off, ...)          int32 ACTION with packed reductions (packed_action)
 constexpr size_t kTableOff = 256;
 constexpr size_t kArgmaxBytes = 65536 * sizeof(unsigned long long);
 
@@ -93,12 +94,18 @@ struct psc_handle {
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
-    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0;
+    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0;
+    bool action_packed = false;    // the device ACTION copy carries each reduction's length and lhs
     size_t device_bytes_needed() const;
 };
 
 namespace psc {
 void set_error(const std::string &msg);
+// ACTION as the device advance reads it: a reduction's entry carries the
+// production's length and left-hand side, kind | len << 2 | lhs << 10, so a
+// reduction needs no second table read.  Returns false (and leaves `out`
+// empty) when some production does not fit (length > 255 or lhs >= 2^21).
+bool packed_action(const psc_handle &h, std::vector<int32_t> &out);
 // The input checks of psc_build (ids in range, spellings), for loaded tables.
 psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg);
 }

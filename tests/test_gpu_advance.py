@@ -173,3 +173,34 @@ def test_loaded_classifier_on_device(built, tmp_path):
         t = torch.from_numpy(rng.integers(0, wl.V, len(states)).astype(np.int32)).to(DEV)
         assert torch.equal(d1.advance(t), d2.advance(t))
         assert _same_states(d1.host_states(), d2.host_states()) < 0
+
+
+def test_advance_long_production():
+    """A production longer than the packed ACTION encoding holds (300
+    symbols): the advance reads its length and left-hand side from the
+    production tables instead, and still matches the oracle step by step."""
+    from inputs.grammar import Grammar
+    from inputs.vocab import Vocab
+    from paper_2608_03065_amd.psc import Classifier
+    n = 300
+    g = Grammar("doc")
+    g.ignore("WS", " +")
+    g.rule("doc", " ".join(['"a"'] * n), '"c"')
+    gt = g.compile()
+    vocab = Vocab(tokens=[b"a", b"aa", b"aaaa", b" ", b"c", b"ac", b""], eos_id=6)
+    clf = Classifier(gt, vocab).bind(DEV)
+    orc = Oracle(gt, vocab)
+    text = b"a" * (n - 7) + b" aa" + b"aaaa" + b"a"
+    toks = vocab.tokenize(text) + [vocab.eos_id]
+    cap = n + 8
+    ds = DecodeStates(clf, 2, cap, DEV)
+    want = ds.host_states()
+    for k, t in enumerate(toks):
+        tt = np.array([t, 4 if k == 0 else t], np.int32)    # the second sequence takes "c" first
+        st = ds.advance(torch.from_numpy(tt).to(DEV)).cpu().numpy()
+        exp_st, want = _oracle_step(orc, want, tt, cap)
+        assert np.array_equal(st, exp_st), (k, st, exp_st)
+        assert _same_states(ds.host_states(), want) < 0, k
+        if k % 50 == 0:
+            assert np.array_equal(ds.compute_masks().cpu().numpy().view(np.uint32), orc.masks(want)), k
+    assert st[0] == psc.ADV_EOS
