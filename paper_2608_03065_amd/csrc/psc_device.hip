@@ -58,7 +58,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *p, uint3
 //   sparse row: lane 0 <- (end_class, n_edges), lane 1 <- (default, -),
 //               lane j >= 2 <- edge j-2 as (symbol, ref); the edge matching
 //               the symbol is found with a ballot and read with readlane;
-//   dense row:  lane 0 <- (end_class, -), lane 1 <- entry[symbol];
+//   dense row:  entry[symbol] (or the end class) by a scalar load;
 //   chain:      lane j <- the j-th entry from the current state; lane j
 //               compares it with the j-th next stack symbol (a cross-lane
 //               shuffle of the staged window), and a ballot finds the first
@@ -120,20 +120,14 @@ struct Walk {
     }
 
     // One step from a sparse row (lane 0: end_class, n_edges; lane 1:
-    // default; lane j >= 2: edge j-2) or a dense row (lane 0: end_class;
-    // lane 1: the aligned pair holding entry X).
-    __device__ __forceinline__ bool row_step(const int2 v, bool dense, int X) {
+    // default; lane j >= 2: edge j-2).
+    __device__ __forceinline__ bool row_step(const int2 v, int X) {
         const int va = v.x, vc = v.y;
         if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); return true; }
-        int nref;
-        if (dense) {
-            nref = (X & 1) ? __builtin_amdgcn_readlane(vc, 1) : __builtin_amdgcn_readlane(va, 1);
-        } else {
-            const int n = __builtin_amdgcn_readlane(vc, 0);
-            const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
-            nref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
-                       : __builtin_amdgcn_readlane(va, 1);
-        }
+        const int n = __builtin_amdgcn_readlane(vc, 0);
+        const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
+        const int nref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
+                             : __builtin_amdgcn_readlane(va, 1);
         // a symbol out of range ends the walk through kRefFault; a select,
         // not a branch, so that the row load cannot sink below the window
         ref = X >= 0 && X < n_lr ? nref : kRefFault;
@@ -147,14 +141,18 @@ struct Walk {
         const int32_t *row = table + (ref & ~3);
         if ((ref & 3) == kRefChain) return chain_step(*reinterpret_cast<const int4 *>(row + kChainEntry * lane));
         if ((ref & 3) == kRefDense) {
-            const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+            // one uniform address: a scalar load
+            if (i < 0) { cls = row[0]; return true; }
+            const int X = __builtin_amdgcn_readlane(sym, chunk_base - i);
             const int Xd = X >= 0 && X < n_lr ? X : 0;
-            const int2 v = *reinterpret_cast<const int2 *>(row + (lane == 0 ? 0 : kRowHeader + (Xd & ~1)));
-            return row_step(v, true, X);
+            const int nref = row[kRowHeader + Xd];
+            ref = X >= 0 && X < n_lr ? nref : kRefFault;
+            i--;
+            return false;
         }
         const int2 v = *reinterpret_cast<const int2 *>(row + 2 * lane);
         const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
-        return row_step(v, false, X);
+        return row_step(v, X);
     }
 };
 
