@@ -46,6 +46,11 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
 constexpr int32_t kRsrcWord3 = 0x00020000;
 constexpr uint32_t kOffSkip = 0x80000000u;   // an offset past any resource used here
 constexpr int kPolicyNt = 2;                  // cache policy: nontemporal (streaming)
+// Stores of logits: nontemporal at device scope (sc1), so that they are
+// written through the XCD's L2 instead of staying dirty in it until the end
+// of the kernel (1% faster steps than nontemporal alone on every workload;
+// without nontemporal, 13-15% slower).
+constexpr int kPolicyStore = kPolicyNt | 16;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t wave_rsrc(const void *p, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int32_t)bytes, kRsrcWord3);
@@ -323,7 +328,7 @@ __device__ __forceinline__ void apply_words(uint4 *__restrict__ base, uint32_t b
                 if (!((g[j] >> k) & 1)) val[k] = kF32NegInf;
         }
         const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
-        __builtin_amdgcn_raw_buffer_store_b128(val, rsrc, g[j] != kFull ? off : kOffSkip, 0, kPolicyNt);
+        __builtin_amdgcn_raw_buffer_store_b128(val, rsrc, g[j] != kFull ? off : kOffSkip, 0, kPolicyStore);
     }
 }
 
