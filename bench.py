@@ -172,6 +172,51 @@ def main():
 
         t_argmax = loop(argmax_step, 1000)
 
+        # the classification step alone (psc_compute_classes: the walk, one
+        # wavefront per sequence, class ids out)
+        cls_out = torch.empty(B, dtype=torch.int32, device=dev)
+
+        def classes_step(i):
+            stacks, lens, qs = step_inputs[i % n_distinct]
+            clf.compute_classes(stacks, lens, qs, out=cls_out, stream=stream)
+
+        # a call this short is bound by the host when launched eagerly, so
+        # 100 of them are captured in a HIP graph and replayed
+        t_walk_eager = loop(classes_step, 1000)
+        g_walk = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_walk, stream=stream):
+            for i in range(100):
+                classes_step(i)
+        g_walk.replay()
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(10):
+            g_walk.replay()
+        z.record(stream)
+        torch.cuda.synchronize()
+        t_walk = a.elapsed_time(z) / 1000 * 1e3
+        del g_walk
+
+        # inputs handed over from pinned host memory: the copies alone, and
+        # copies + the step (PCIe-inclusive; never the headline)
+        host_in = []
+        for s_ in range(min(n_distinct, 8)):
+            host_in.append(tuple(t.cpu().pin_memory() for t in step_inputs[s_]))
+        dev_in = [tuple(torch.empty(h.shape, dtype=h.dtype, device=dev) for h in hs) for hs in host_in]
+
+        def upload(i):
+            for d, h in zip(dev_in[i % len(host_in)], host_in[i % len(host_in)]):
+                d.copy_(h, non_blocking=True)
+
+        def upload_step(i):
+            upload(i)
+            stacks, lens, qs = dev_in[i % len(host_in)]
+            clf.compute_and_apply(stacks, lens, qs, pool[i % n_pool], out=bms[i % n_bm], stream=stream)
+
+        t_upload = loop(upload, 1000)
+        t_upload_step = loop(upload_step, 1000)
+
         # the timed step captured in a HIP graph: G steps (rotating inputs
         # and logits as above) per graph, replayed back to back
         G = 100
@@ -265,7 +310,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, step_states, args.cpu_seconds, B)
+        cpu = cpu_baseline(wl, step_states, args.cpu_seconds, B, clf)
 
     out = {
         "metric": METRIC,
@@ -291,6 +336,15 @@ def main():
         "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
         "decode_step_us": decode,
         "argmax_step_us": round(t_argmax, 3),
+        "walk_us": {"graph_replayed": round(t_walk, 3), "eager": round(t_walk_eager, 3),
+                    "call": "psc_compute_classes (the walk alone, class ids out)"},
+        "stack_depth": {"mean": round(float(np.mean(depth_hist)), 2),
+                        "p50": int(np.percentile(depth_hist, 50)), "p90": int(np.percentile(depth_hist, 90)),
+                        "p99": int(np.percentile(depth_hist, 99)), "max": int(max(depth_hist)),
+                        "hist": depth_histogram(depth_hist)},
+        "host_inputs": {"upload_us": round(t_upload, 3), "upload_and_step_us": round(t_upload_step, 3),
+                        "note": "stacks, lengths and lexer states copied from pinned host memory on the "
+                                "bench stream before the step; PCIe-inclusive, not the headline"},
         "graph_step_us": round(t_graph, 3),
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
                        "apply_mask_solo_gbs": round(achieved_apply, 1)},
@@ -383,8 +437,23 @@ def measured_traffic(workload: str, kernel: str):
     return meta["kernels"][kernel]["hbm_bytes"]
 
 
-def cpu_baseline(wl, step_states, seconds, B):
-    """The oracle as it stands, on this host's cores, over a bounded sample."""
+def depth_histogram(depths):
+    """Counts of stack depths in power-of-two bins [2^k, 2^(k+1))."""
+    import numpy as np
+    d = np.asarray(depths)
+    out = {}
+    k = 1
+    while k <= d.max():
+        out[f"{k}-{2 * k - 1}"] = int(((d >= k) & (d < 2 * k)).sum())
+        k *= 2
+    return out
+
+
+def cpu_baseline(wl, step_states, seconds, B, clf):
+    """The oracle as it stands, on this host's cores, over a bounded sample;
+    beside it, the oracle on one thread (ns per token check) and the paper's
+    own CPU method (the host walk of the same classifier plus the copy of the
+    class's mask row, one thread, per sequence)."""
     import numpy as np
 
     from oracle import Oracle
@@ -398,11 +467,44 @@ def cpu_baseline(wl, step_states, seconds, B):
     t0 = time.time()
     orc.masks(flat[:n])
     dt = time.time() - t0
+    cores = int(orc.threads_used)
+    # one thread
+    t0 = time.time()
+    orc.masks(flat[:1], n_threads=1)
+    one1 = time.time() - t0
+    n1 = int(max(1, min(len(flat), 2.0 / max(one1, 1e-4))))
+    t0 = time.time()
+    orc.masks(flat[:n1], n_threads=1)
+    dt1 = time.time() - t0
+    # the paper's method on one CPU thread: walk, then the mask row copy
+    sample = flat[:min(len(flat), 4096)]
+    classes = clf.classify_host(sample)
+    rows = {int(c): clf.class_mask(int(c)) for c in np.unique(classes)}
+    table = np.zeros((max(rows) + 1, clf.W), np.uint32)
+    for c, r in rows.items():
+        table[c] = r
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        c = clf.classify_host(sample)
+        out = table[c]
+        reps += 1
+        if time.perf_counter() - t0 > 1.0:
+            break
+    t_psc = (time.perf_counter() - t0) / (reps * len(sample))
+    del out
     return {
-        "value": round(n / dt, 3), "unit": "masks/s", "cores": int(orc.threads_used), "kind": "oracle",
+        "value": round(n / dt, 3), "unit": "masks/s", "cores": cores, "kind": "oracle",
         "sample": f"first {n} sequences (of {len(flat)}) of the benchmark's prefix batches, "
                   f"all {wl.V} tokens each; {dt:.1f}s wall",
         "per_step_latency_us": round(dt / n * B * 1e6, 1),
+        "single_thread_ns_per_token_check": round(dt1 / (n1 * wl.V) * 1e9, 2),
+        "single_thread_sample": f"first {n1} sequences, {dt1:.1f}s",
+        "paper_method_cpu_us_per_sequence": round(t_psc * 1e6, 3),
+        "paper_method_note": "host walk of the same classifier (psc_classify_host) plus a copy of the "
+                             "class's mask row, one thread, over the first "
+                             f"{len(sample)} sequences; the paper reports 2.2-2.6 us per token on one "
+                             "Xeon Gold 6348 thread (Python)",
     }
 
 

@@ -194,6 +194,19 @@ psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask
                           int32_t V, void *stream);
 
 /*
+ * The classification step of Algorithm 2 alone: out_classes[b] = the class
+ * of sequence b, i.e. the row of the precomputed mask table that
+ * psc_compute_masks would copy (psc_class_mask_host returns that row on the
+ * host).  Inputs as for psc_compute_masks; out_classes is device int32 [B].
+ * An out-of-range input gives -1 and increments the device error counter.
+ * For callers that share or cache masks by class, and to time the walk on
+ * its own.  B == 0 is a no-op.  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND,
+ * PSC_E_DEVICE.
+ */
+psc_status psc_compute_classes(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                               const int32_t *lexer_states, int32_t B, int32_t *out_classes, void *stream);
+
+/*
  * The whole per-step path in one launch: psc_compute_masks followed by
  * psc_apply_mask (Algorithm 2, classification and mask steps; Sec. 1,
  * Fig. 1a), fused so that each workgroup walks its sequence, gathers its
@@ -284,6 +297,11 @@ psc_status psc_advance(const psc_handle *h, int32_t *stacks, int32_t cap, int32_
 psc_status psc_compute_masks_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
                                    const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
                                    uint32_t *out_bitmask, void *stream);
+
+/* psc_compute_classes on device-resident states (dense layout above). */
+psc_status psc_compute_classes_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                     const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                     int32_t *out_classes, void *stream);
 
 /* psc_compute_and_apply on device-resident states (dense layout above). */
 psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,

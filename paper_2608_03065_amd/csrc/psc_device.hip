@@ -189,6 +189,24 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
 // counts rejected inputs.  Round trip 1 fetches lens[b], qs[b] and, for
 // ragged stacks (stride 0), the lengths before b (the stack's offset); with
 // stride > 0 stack b starts at b * stride and holds at most stride symbols.
+__device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
+                                          const int32_t *__restrict__ stacks, int32_t stride,
+                                          const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
+                                          int b, int lane) {
+    const int own = *((lane & 1) ? qs + b : lens + b);
+    int part = 0;
+    if (stride == 0) {
+        part = lane < b ? lens[lane] : 0;
+        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+    }
+    const int len = __builtin_amdgcn_readlane(own, 0);
+    const int q = __builtin_amdgcn_readlane(own, 1);
+    const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
+    if (len > 0 && (stride == 0 || len <= stride) && q >= 0 && q < n_lex)
+        return walk_class(table, n_lr, stacks + off, len, q, lane);
+    return -1;
+}
+
 __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                            const int32_t *__restrict__ stacks, int32_t stride,
                                            const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
@@ -196,18 +214,7 @@ __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, in
     __shared__ int32_t s_cls;
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
-        const int own = *((lane & 1) ? qs + b : lens + b);
-        int part = 0;
-        if (stride == 0) {
-            part = lane < b ? lens[lane] : 0;
-            for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
-        }
-        const int len = __builtin_amdgcn_readlane(own, 0);
-        const int q = __builtin_amdgcn_readlane(own, 1);
-        const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
-        int cls = -1;
-        if (len > 0 && (stride == 0 || len <= stride) && q >= 0 && q < n_lex)
-            cls = walk_class(table, n_lr, stacks + off, len, q, lane);
+        const int cls = wave_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, lane);
         if (lane == 0) {
             s_cls = cls;
             if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
@@ -215,6 +222,22 @@ __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, in
     }
     __syncthreads();
     return s_cls;
+}
+
+// psc_compute_classes: the walk alone (Algorithm 2, classification step),
+// one wavefront per sequence, kBlock / kWave sequences per workgroup.
+__global__ void __launch_bounds__(kBlock)
+classes_kernel(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+               int32_t stride, const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t B,
+               int32_t *__restrict__ out, uint32_t *__restrict__ err) {
+    const int b = blockIdx.x * (kBlock / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    if (b >= B) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int cls = wave_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, lane);
+    if (lane == 0) {
+        out[b] = cls;
+        if (cls < 0) atomicAdd(err, 1u);
+    }
 }
 
 // One workgroup per (sequence b, slice of the mask row): the walk, then the
@@ -732,6 +755,26 @@ psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t st
     return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }
 
+// The walk alone for ragged (stride 0) or strided stacks.
+psc_status launch_classes(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
+                          const int32_t *lexer_states, int32_t B, int32_t *out_classes, void *stream,
+                          const char *what) {
+    if (psc_status st = check_bound(h, what)) return st;
+    if (B < 0 || stride < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_classes))) {
+        set_error(std::string(what) + ": null argument or negative size");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    char *base = static_cast<char *>(h->dev_base);
+    const int per_block = kBlock / kWave;
+    hipLaunchKernelGGL(classes_kernel, dim3((B + per_block - 1) / per_block), dim3(kBlock), 0,
+                       reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const int32_t *>(base + kTableOff),
+                       h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, B, out_classes,
+                       reinterpret_cast<uint32_t *>(base));
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+}
+
 // The single-launch step for ragged (stride 0) or strided stacks.
 psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
                         const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
@@ -902,6 +945,21 @@ extern "C" psc_status psc_compute_masks(const psc_handle *h, const int32_t *stac
                                         const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
                                         void *stream) {
     return launch_compute(h, stacks, 0, stack_lens, lexer_states, B, out_bitmask, stream, "psc_compute_masks");
+}
+
+extern "C" psc_status psc_compute_classes(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
+                                          const int32_t *lexer_states, int32_t B, int32_t *out_classes,
+                                          void *stream) {
+    return launch_classes(h, stacks, 0, stack_lens, lexer_states, B, out_classes, stream, "psc_compute_classes");
+}
+
+extern "C" psc_status psc_compute_classes_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
+                                                const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                                int32_t *out_classes, void *stream) {
+    if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_classes_dense"))
+        return st;
+    return launch_classes(h, stacks, cap, stack_lens, lexer_states, B, out_classes, stream,
+                          "psc_compute_classes_dense");
 }
 
 extern "C" psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,

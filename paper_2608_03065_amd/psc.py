@@ -22,7 +22,7 @@ _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
             "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
             "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_compute_and_argmax",
-            "psc_compute_and_argmax_dense", "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_compute_and_argmax_dense", "psc_compute_classes", "psc_compute_classes_dense", "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -83,6 +83,8 @@ def lib() -> C.CDLL:
         L.psc_compute_and_apply.argtypes = [P, P, P, P, I32, P, P, C.c_int, I32, P]
         L.psc_compute_and_argmax.argtypes = [P, P, P, P, I32, P, C.c_int, I32, P, P]
         L.psc_compute_and_argmax_dense.argtypes = [P, P, I32, P, P, I32, P, C.c_int, I32, P, P]
+        L.psc_compute_classes.argtypes = [P, P, P, P, I32, P, P]
+        L.psc_compute_classes_dense.argtypes = [P, P, I32, P, P, I32, P, P]
         L.psc_save.argtypes = [P, C.c_char_p]
         L.psc_load.argtypes = [C.c_char_p, C.POINTER(P)]
         L.psc_state_reset.argtypes = [P, P, I32, P, P, I32, P]
@@ -98,7 +100,7 @@ def lib() -> C.CDLL:
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
                      "psc_compute_and_apply_dense", "psc_compute_and_argmax", "psc_compute_and_argmax_dense",
-                     "psc_save", "psc_load", "psc_device_error_count",
+                     "psc_compute_classes", "psc_compute_classes_dense", "psc_save", "psc_load", "psc_device_error_count",
                      "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -235,6 +237,19 @@ class Classifier:
                                        lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
 
+    def compute_classes(self, stacks, stack_lens, lexer_states, out=None, stream=None):
+        """Device int32 tensors -> class ids int32 [B] (-1 for a rejected input)."""
+        import torch
+        B = int(stack_lens.shape[0])
+        for t in (stacks, stack_lens, lexer_states):
+            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
+        if out is None:
+            out = torch.empty(B, dtype=torch.int32, device=stack_lens.device)
+        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and out.numel() == B
+        _check(lib().psc_compute_classes(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
+                                         lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
+        return out
+
     def compute_and_apply(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
         """One launch: masks for the B prefix states applied to logits [B, V] in
         place; the bitmask is also written to `out` when given.  Returns logits."""
@@ -325,6 +340,15 @@ class DecodeStates:
         assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
         _check(lib().psc_compute_masks_dense(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
                                              self.qs.data_ptr(), self.B, out.data_ptr(), _stream_ptr(stream)))
+        return out
+
+    def compute_classes(self, out=None, stream=None):
+        import torch
+        if out is None:
+            out = torch.empty(self.B, dtype=torch.int32, device=self.lens.device)
+        assert out.is_contiguous() and out.numel() == self.B and out.dtype == torch.int32
+        _check(lib().psc_compute_classes_dense(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
+                                               self.qs.data_ptr(), self.B, out.data_ptr(), _stream_ptr(stream)))
         return out
 
     def compute_and_apply(self, logits, out=None, stream=None):

@@ -151,3 +151,39 @@ def test_apply_after_compute_end_to_end(built, name, step):
     torch.cuda.synchronize()
     want = _closed_form(logits, orc.masks(states), wl.V)
     assert torch.equal(_as_int(dev.cpu()), _as_int(want))
+
+
+@pytest.mark.parametrize("name,steps", [("arithmetic", range(0, 200, 7)), ("json", range(0, 40, 5)),
+                                        ("schema", [0, 333, 999]), ("pylike", [2, 222]), ("stress", [5, 555])])
+def test_classes_match_host_walk_and_masks(built, name, steps):
+    """psc_compute_classes (ragged and dense) gives the host walk's class,
+    and that class's mask row is the oracle's mask."""
+    from paper_2608_03065_amd.psc import DecodeStates
+    wl, clf, orc = built(name)
+    clf.error_count(reset=True)
+    for step in steps:
+        states = wl.states(step)
+        stacks, lens, qs = pack_states(states, DEV)
+        got = clf.compute_classes(stacks, lens, qs).cpu().numpy()
+        assert np.array_equal(got, clf.classify_host(states)), step
+        cap = max(len(a) for _, a in states) + 3
+        dense = DecodeStates(clf, len(states), cap, DEV).load(states).compute_classes().cpu().numpy()
+        assert np.array_equal(dense, got), step
+        want = orc.masks(states[:4])
+        for b in range(len(want)):
+            assert np.array_equal(clf.class_mask(int(got[b])), want[b]), (step, b)
+    assert clf.error_count() == 0
+
+
+def test_classes_reject_out_of_range(built):
+    wl, clf, _ = built("arithmetic")
+    clf.error_count(reset=True)
+    good = wl.states(3)[0]
+    n_lr = wl.grammar.n_lr_states
+    states = [good, (wl.grammar.lexer.n_states, good[1]),
+              (good[0], np.concatenate([good[1][:-1], [n_lr]]).astype(np.int32)), good]
+    stacks, lens, qs = pack_states(states, DEV)
+    got = clf.compute_classes(stacks, lens, qs).cpu().numpy()
+    want = clf.classify_host([good])[0]
+    assert got.tolist() == [want, -1, -1, want]
+    assert clf.error_count(reset=True) == 2
