@@ -175,17 +175,19 @@ def test_loaded_classifier_on_device(built, tmp_path):
         assert _same_states(d1.host_states(), d2.host_states()) < 0
 
 
-def test_advance_long_production():
+@pytest.mark.parametrize("fillers", [0, 600])
+def test_advance_long_production(fillers):
     """A production longer than the packed ACTION encoding holds (300
     symbols): the advance reads its length and left-hand side from the
-    production tables instead, and still matches the oracle step by step."""
+    production tables instead, and still matches the oracle step by step,
+    also with 600 more alternatives (parser tables of about 1 MB)."""
     from inputs.grammar import Grammar
     from inputs.vocab import Vocab
     from paper_2608_03065_amd.psc import Classifier
     n = 300
     g = Grammar("doc")
     g.ignore("WS", " +")
-    g.rule("doc", " ".join(['"a"'] * n), '"c"')
+    g.rule("doc", " ".join(['"a"'] * n), '"c"', *[f'"x{i}"' for i in range(fillers)])
     gt = g.compile()
     vocab = Vocab(tokens=[b"a", b"aa", b"aaaa", b" ", b"c", b"ac", b""], eos_id=6)
     clf = Classifier(gt, vocab).bind(DEV)
