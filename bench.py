@@ -388,33 +388,40 @@ def decode_steps(wl, clf, B, pool, bms, stream, dev, max_steps):
     ds = DecodeStates(clf, B, cap, dev, stream)
     n_pool, n_bm = len(pool), len(bms)
 
-    def run(with_masks):
+    def run(mode):
         a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ds.reset(stream)
         torch.cuda.synchronize()
         a.record(stream)
         for k in range(n):
+            if mode == "one_launch":
+                ds.decode_step(tok_dev[k], pool[k % n_pool], out=bms[k % n_bm], stream=stream)
+                continue
             ds.advance(tok_dev[k], stream)
-            if with_masks:
+            if mode == "two_launches":
                 ds.compute_and_apply(pool[k % n_pool], out=bms[k % n_bm], stream=stream)
         z.record(stream)
         torch.cuda.synchronize()
         return a.elapsed_time(z) / n * 1e3
 
-    run(True)
-    t_both = run(True)
-    t_adv = run(False)
-    # the states after n tokens equal the host parser's at the same cut
-    got = ds.host_states()
-    ok = True
-    for b in range(B):
-        cut = sum(len(wl.vocab.tokens[t]) for t in toks[b][:n])
-        q, st = wl.host.states_at(texts[b], [cut])[0]
-        ok &= got[b][0] == q and np.array_equal(got[b][1], st)
-    if not ok:
-        raise RuntimeError("device states after the decoding loop differ from the host parser's")
-    return {"advance_and_fused_step": round(t_both, 3), "advance": round(t_adv, 3), "tokens_per_sequence": n,
-            "cap": cap, "states_checked": True}
+    def check():
+        # the states after n tokens equal the host parser's at the same cut
+        got = ds.host_states()
+        for b in range(B):
+            cut = sum(len(wl.vocab.tokens[t]) for t in toks[b][:n])
+            q, st = wl.host.states_at(texts[b], [cut])[0]
+            if got[b][0] != q or not np.array_equal(got[b][1], st):
+                raise RuntimeError("device states after the decoding loop differ from the host parser's")
+
+    run("two_launches")
+    t_both = run("two_launches")
+    check()
+    t_one = run("one_launch")
+    check()
+    t_adv = run("advance")
+    check()
+    return {"advance_and_fused_step": round(t_both, 3), "decode_step_one_launch": round(t_one, 3),
+            "advance": round(t_adv, 3), "tokens_per_sequence": n, "cap": cap, "states_checked": True}
 
 
 def measured_traffic(workload: str, kernel: str):

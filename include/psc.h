@@ -309,6 +309,32 @@ psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stack
                                        uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
                                        void *stream);
 
+/*
+ * One whole decoding step of Algorithm 2 in one launch, on device-resident
+ * states: the lexing and parsing steps (psc_advance by tokens[b]), then the
+ * classification and mask steps of the new state, applied to the logits
+ * (psc_compute_and_apply_dense).  The results (new states, status, bitmask,
+ * masked logits, error counter) are bit-identical to copying each state to
+ * the output buffers, calling psc_advance on them, then
+ * psc_compute_and_apply_dense.
+ *  stacks_in, lens_in, qs_in     device, the current states (dense layout
+ *                                above, `cap`); only read.
+ *  stacks_out, lens_out, qs_out  device, the same shapes: receive the new
+ *                                states (a state that does not advance is
+ *                                copied unchanged).  They must not overlap the
+ *                                inputs (checked): every workgroup of a
+ *                                sequence reads the old state while one writes
+ *                                the new one, so callers alternate two buffers.
+ *  tokens, status                as for psc_advance.
+ *  out_bitmask, logits, dtype, V as for psc_compute_and_apply.
+ * B == 0 is a no-op.  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND,
+ * PSC_E_DEVICE.
+ */
+psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks_in, const int32_t *lens_in,
+                           const int32_t *qs_in, int32_t *stacks_out, int32_t *lens_out, int32_t *qs_out,
+                           int32_t cap, int32_t B, const int32_t *tokens, int32_t *status,
+                           uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V, void *stream);
+
 /* psc_compute_and_argmax on device-resident states (dense layout above). */
 psc_status psc_compute_and_argmax_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
                                         const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,

@@ -80,6 +80,9 @@ static_assert(kChainMax <= kChunk, "a chain must end within one wavefront load")
 
 constexpr int32_t kRefFault = INT32_MIN;   // no class ref is this small
 
+// With kOverlay, stack indices >= ptr are read from `ov` (the states a
+// token pushed, in LDS, not yet written to memory) instead of `st`.
+template <bool kOverlay = false>
 struct Walk {
     const int32_t *__restrict__ table;
     const int32_t *__restrict__ st;
@@ -90,8 +93,14 @@ struct Walk {
     int sym;          // the window (lanes past the bottom hold st[0], never used)
     int ref;          // current state (wave-uniform)
     int cls;          // the result once the walk has ended
+    const int32_t *ov = nullptr;
+    int ptr = 0;
 
-    __device__ __forceinline__ void stage() { sym = st[max(chunk_base - lane, 0)]; }
+    __device__ __forceinline__ int load(int idx) const {
+        if (kOverlay && idx >= ptr) return ov[idx - ptr];
+        return st[idx];
+    }
+    __device__ __forceinline__ void stage() { sym = load(max(chunk_base - lane, 0)); }
 
     // One step from a chain entry: lane j holds the j-th entry from the
     // current state.  Returns true when the walk has ended.
@@ -161,11 +170,13 @@ struct Walk {
     }
 };
 
+template <bool kOverlay = false>
 __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lr,
-                                          const int32_t *__restrict__ st, int len, int q, int lane) {
-    Walk w{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1};
+                                          const int32_t *__restrict__ st, int len, int q, int lane,
+                                          const int32_t *ov = nullptr, int ptr = 0) {
+    Walk<kOverlay> w{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1, ov, ptr};
     // round trip 2: the window, with start[q] in lane 63
-    w.sym = lane == kChunk ? table[q] : st[max(w.chunk_base - lane, 0)];
+    w.sym = lane == kChunk ? table[q] : w.load(max(w.chunk_base - lane, 0));
     w.ref = __builtin_amdgcn_readlane(w.sym, kChunk);
     if (w.ref < 0) return -w.ref - 1;
     if (w.step()) return w.cls;
@@ -402,15 +413,13 @@ apply_generic_kernel(void *__restrict__ logits, const uint32_t *__restrict__ bit
 // latency but no bandwidth.
 constexpr int kFusedBlock = 4 * kWave;
 
+// The part of the fused step after the walk: this workgroup's slice of the
+// class's mask row, written to out_bitmask[b] and applied to logits[b].
 template <bool kBf16>
-__global__ void __launch_bounds__(kFusedBlock)
-fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
-                  const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
-                  uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
+__device__ __forceinline__ void fused_fast_apply(int cls, int b, const uint32_t *__restrict__ masks,
+                                                 int32_t mask_stride, int32_t W, uint32_t *__restrict__ out,
+                                                 uint4 *__restrict__ logits) {
     using G = ApplyGeom<kBf16>;
-    const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1);
     const int w_base =
         (blockIdx.x * (kFusedBlock / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave)) * G::kWordsPerWave;
@@ -426,6 +435,17 @@ fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict_
     if (out && mine) out[(size_t)b * W + w] = m;
 }
 
+template <bool kBf16>
+__global__ void __launch_bounds__(kFusedBlock)
+fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
+                  const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
+                  uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
+    const int b = blockIdx.y;
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
+    fused_fast_apply<kBf16>(cls, b, masks, mask_stride, W, out, logits);
+}
+
 // psc_compute_and_apply, general path (any V, any element alignment): one
 // workgroup per (sequence b, kGenWords mask words); the words go through LDS
 // and each thread then masks single elements.
@@ -433,14 +453,10 @@ constexpr int kGenWords = 128;
 static_assert(kGenWords <= kBlock, "one pass stages the slice's words");
 
 template <bool kBf16>
-__global__ void __launch_bounds__(kBlock)
-fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
-                     const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
-                     uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
+__device__ __forceinline__ void fused_generic_apply(int cls, int b, const uint32_t *__restrict__ masks,
+                                                    int32_t mask_stride, int32_t V, int32_t W,
+                                                    uint32_t *__restrict__ out, void *__restrict__ logits) {
     __shared__ uint32_t s_m[kGenWords];
-    const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
     const int w0 = blockIdx.x * kGenWords;
     const int nw = min(kGenWords, W - w0);
     if (threadIdx.x < nw) {
@@ -456,6 +472,17 @@ fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restri
         if (kBf16) reinterpret_cast<uint16_t *>(logits)[idx] = kBf16NegInf;
         else reinterpret_cast<uint32_t *>(logits)[idx] = kF32NegInf;
     }
+}
+
+template <bool kBf16>
+__global__ void __launch_bounds__(kBlock)
+fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
+                     const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
+                     uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
+    const int b = blockIdx.y;
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
+    fused_generic_apply<kBf16>(cls, b, masks, mask_stride, V, W, out, logits);
 }
 
 // ---------------------------------------------------------------- masked argmax
@@ -587,24 +614,20 @@ constexpr int kFeedSteps = 1 << 16;    // bound on the LR steps of one terminal
 // success the overlay is written above ptr.  A terminal is fed as the LR
 // parser does: the reductions its lookahead selects, then a shift (accept
 // for $end); popping the whole stack or a missing goto rejects.
-__global__ void __launch_bounds__(kWave)
-advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ lens,
-               int32_t *__restrict__ qs, int32_t B, const int32_t *__restrict__ tokens,
-               int32_t *__restrict__ status) {
-    __shared__ int32_t s_ov[kOverlay];
-    const int b = blockIdx.x;
-    const int lane = threadIdx.x;
-    const int tok = tokens[b];
-    if (tok < 0) {
-        if (lane == 0) status[b] = PSC_ADV_SKIPPED;
-        return;
-    }
-    const int len = lens[b], q_in = qs[b];
-    if (tok >= T.V || len < 1 || len > cap || q_in < 0 || q_in >= T.n_lex) {
-        if (lane == 0) status[b] = PSC_ADV_BAD_INPUT;
-        return;
-    }
-    const int32_t *st = stacks + (int64_t)b * cap;
+//
+// advance_core computes the outcome of token `tok` on the state (q_in, st
+// of `len` symbols, at most `cap`) and writes nothing but the overlay: on
+// PSC_ADV_OK the new state is st[0 .. ptr) followed by s_ov[0 .. ov), in
+// lexer state q; on any other status the state is unchanged (ptr = len,
+// ov = 0, q = q_in).
+__device__ __forceinline__ int advance_core(const AdvTables &T, int32_t *s_ov, const int32_t *__restrict__ st,
+                                            int len, int q_in, int tok, int cap, int lane, int &ptr_out,
+                                            int &ov_out, int &q_out) {
+    ptr_out = len;
+    ov_out = 0;
+    q_out = q_in;
+    if (tok < 0) return PSC_ADV_SKIPPED;
+    if (tok >= T.V || len < 1 || len > cap || q_in < 0 || q_in >= T.n_lex) return PSC_ADV_BAD_INPUT;
     int ptr = len, ov = 0;
     int32_t cur = st[ptr - 1];   // the top of the stack, kept in a register
     auto reload = [&]() { cur = __builtin_amdgcn_readfirstlane(ov > 0 ? s_ov[ov - 1] : st[ptr - 1]); };
@@ -665,8 +688,7 @@ advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *
             const int r = feed(T.end_term);
             if (r != PSC_ADV_OK) res = r;
         }
-        if (lane == 0) status[b] = res;
-        return;
+        return res;
     }
     // longest match with one byte of lookahead: a byte the pending lexeme
     // cannot take ends it (it must be accepting) and starts the next from q0
@@ -690,6 +712,27 @@ advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *
     }
     if (res == PSC_ADV_OK && ptr + ov > cap) res = PSC_ADV_OVERFLOW;
     if (res == PSC_ADV_OK) {
+        ptr_out = ptr;
+        ov_out = ov;
+        q_out = q;
+    }
+    return res;
+}
+
+// psc_advance: one workgroup of one wavefront per sequence, the state
+// updated in place.
+__global__ void __launch_bounds__(kWave)
+advance_kernel(AdvTables T, int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ lens,
+               int32_t *__restrict__ qs, int32_t B, const int32_t *__restrict__ tokens,
+               int32_t *__restrict__ status) {
+    __shared__ int32_t s_ov[kOverlay];
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int tok = tokens[b];
+    const int len = tok < 0 ? 0 : lens[b], q_in = tok < 0 ? 0 : qs[b];
+    int ptr, ov, q;
+    const int res = advance_core(T, s_ov, stacks + (int64_t)b * cap, len, q_in, tok, cap, lane, ptr, ov, q);
+    if (res == PSC_ADV_OK) {
         int32_t *dst = stacks + (int64_t)b * cap + ptr;
         for (int k = lane; k < ov; k += kWave) dst[k] = s_ov[k];
         if (lane == 0) {
@@ -709,6 +752,84 @@ reset_kernel(int32_t *__restrict__ stacks, int32_t cap, int32_t *__restrict__ le
     stacks[(int64_t)b * cap] = 0;
     lens[b] = 1;
     qs[b] = 0;
+}
+
+// ---------------------------------------------------------------- decoding step
+
+// The state a decoding step reads and the one it writes (dense layout,
+// separate buffers: every workgroup of a sequence reads the old state while
+// the first one writes the new state).
+struct DecodeArgs {
+    AdvTables T;
+    const int32_t *stacks_in, *lens_in, *qs_in;
+    int32_t *stacks_out, *lens_out, *qs_out;
+    const int32_t *tokens;
+    int32_t *status;
+    int32_t cap;
+};
+
+// Algorithm 2 for sequence b in one workgroup: wavefront 0 advances the
+// prefix state by tokens[b] (advance_core: the pushed states stay in the LDS
+// overlay), walks the new state (the kept part of the stack from memory,
+// the pushed states from the overlay) and publishes the class; the
+// sequence's first workgroup also writes the new state and the status.  A
+// token that is not advanced leaves the state as it was, and that state is
+// the one classified, exactly as psc_advance followed by
+// psc_compute_and_apply_dense.
+__device__ __forceinline__ int decode_block_class(const int32_t *__restrict__ table, const DecodeArgs &D, int b,
+                                                  uint32_t *__restrict__ err) {
+    __shared__ int32_t s_cls;
+    __shared__ int32_t s_ov[kOverlay];
+    if (threadIdx.x < kWave) {
+        const int lane = threadIdx.x;
+        const int cap = D.cap;
+        const int tok = D.tokens[b];
+        const int len = D.lens_in[b], q_in = D.qs_in[b];
+        const int32_t *st = D.stacks_in + (int64_t)b * cap;
+        int ptr, ov, q;
+        const int res = advance_core(D.T, s_ov, st, len, q_in, tok, cap, lane, ptr, ov, q);
+        const int new_len = res == PSC_ADV_OK ? ptr + ov : len;
+        if (blockIdx.x == 0) {
+            int32_t *dst = D.stacks_out + (int64_t)b * cap;
+            const int keep = res == PSC_ADV_OK ? ptr : min(max(len, 0), cap);
+            for (int k = lane; k < keep; k += kWave) dst[k] = st[k];
+            for (int k = lane; k < ov; k += kWave) dst[ptr + k] = s_ov[k];
+            if (lane == 0) {
+                D.lens_out[b] = new_len;
+                D.qs_out[b] = q;
+                D.status[b] = res;
+            }
+        }
+        int cls = -1;
+        if (new_len > 0 && new_len <= cap && q >= 0 && q < D.T.n_lex)
+            cls = walk_class<true>(table, D.T.n_lr, st, new_len, q, lane, s_ov, ptr);
+        if (lane == 0) {
+            s_cls = cls;
+            if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
+        }
+    }
+    __syncthreads();
+    return s_cls;
+}
+
+template <bool kBf16>
+__global__ void __launch_bounds__(kFusedBlock)
+decode_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                   DecodeArgs D, int32_t W, uint32_t *__restrict__ out, uint32_t *__restrict__ err,
+                   uint4 *__restrict__ logits) {
+    const int b = blockIdx.y;
+    const int cls = decode_block_class(table, D, b, err);
+    fused_fast_apply<kBf16>(cls, b, masks, mask_stride, W, out, logits);
+}
+
+template <bool kBf16>
+__global__ void __launch_bounds__(kBlock)
+decode_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                      DecodeArgs D, int32_t V, int32_t W, uint32_t *__restrict__ out, uint32_t *__restrict__ err,
+                      void *__restrict__ logits) {
+    const int b = blockIdx.y;
+    const int cls = decode_block_class(table, D, b, err);
+    fused_generic_apply<kBf16>(cls, b, masks, mask_stride, V, W, out, logits);
 }
 
 psc_status device_fail(const char *what, hipError_t e) {
@@ -890,6 +1011,22 @@ psc_status check_dense(const int32_t *stacks, int32_t cap, const int32_t *lens, 
     return PSC_OK;
 }
 
+// The problem instance in the bound buffer, as the advance reads it.
+AdvTables adv_tables(const psc_handle *h) {
+    const char *base = static_cast<const char *>(h->dev_base);
+    const int32_t *g = reinterpret_cast<const int32_t *>(base + h->gram_off);
+    const psc::AdvanceLayout &L = h->adv;
+    const int32_t *action = h->action_packed ? reinterpret_cast<const int32_t *>(base + h->packed_off) : g + L.action;
+    return AdvTables{g + L.lex_next, g + L.lex_accept, g + L.ignored, action, g + L.go, g + L.prod_lhs,
+                     g + L.prod_len, g + L.tok_off, reinterpret_cast<const uint8_t *>(base + h->vbytes_off),
+                     h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0};
+}
+
+bool ranges_overlap(const void *a, const void *b, size_t n) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + n && y < x + n;
+}
+
 }  // namespace
 
 extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream) {
@@ -1028,18 +1165,72 @@ extern "C" psc_status psc_advance(const psc_handle *h, int32_t *stacks, int32_t 
         return PSC_E_INVALID_ARG;
     }
     if (B == 0) return PSC_OK;
-    const char *base = static_cast<const char *>(h->dev_base);
-    const int32_t *g = reinterpret_cast<const int32_t *>(base + h->gram_off);
-    const psc::AdvanceLayout &L = h->adv;
-    const int32_t *action = h->action_packed ? reinterpret_cast<const int32_t *>(base + h->packed_off) : g + L.action;
-    AdvTables T{g + L.lex_next, g + L.lex_accept, g + L.ignored, action, g + L.go, g + L.prod_lhs,
-                g + L.prod_len, g + L.tok_off, reinterpret_cast<const uint8_t *>(base + h->vbytes_off),
-                h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0};
+    const AdvTables T = adv_tables(h);
     hipLaunchKernelGGL(advance_kernel, dim3(B), dim3(kWave), 0,
                        reinterpret_cast<hipStream_t>(stream), T, stacks, cap, stack_lens, lexer_states, B, tokens,
                        status);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? PSC_OK : device_fail("psc_advance", e);
+}
+
+extern "C" psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks_in, const int32_t *lens_in,
+                                      const int32_t *qs_in, int32_t *stacks_out, int32_t *lens_out, int32_t *qs_out,
+                                      int32_t cap, int32_t B, const int32_t *tokens, int32_t *status,
+                                      uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                      void *stream) {
+    const char *what = "psc_decode_step";
+    if (psc_status st = check_bound(h, what)) return st;
+    if (psc_status st = check_dense(stacks_in, cap, lens_in, qs_in, B, what)) return st;
+    if (psc_status st = check_dense(stacks_out, cap, lens_out, qs_out, B, what)) return st;
+    if (B > 0 && (!tokens || !status || !logits || (dtype != PSC_F32 && dtype != PSC_BF16))) {
+        set_error("psc_decode_step: null tokens, status or logits, or bad dtype");
+        return PSC_E_INVALID_ARG;
+    }
+    if (V != h->V) {
+        set_error("psc_decode_step: V differs from the vocabulary size");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B > 65535) {
+        set_error("psc_decode_step: B > 65535");
+        return PSC_E_INVALID_ARG;
+    }
+    if (B == 0) return PSC_OK;
+    const size_t n_st = (size_t)B * cap * sizeof(int32_t), n_b = (size_t)B * sizeof(int32_t);
+    if (ranges_overlap(stacks_in, stacks_out, n_st) || ranges_overlap(lens_in, lens_out, n_b) ||
+        ranges_overlap(qs_in, qs_out, n_b)) {
+        set_error("psc_decode_step: the input and output states overlap");
+        return PSC_E_INVALID_ARG;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(h->dev_base);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
+    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const DecodeArgs D{adv_tables(h), stacks_in, lens_in, qs_in, stacks_out, lens_out, qs_out, tokens, status, cap};
+    const int32_t W = h->W;
+    const bool bf16 = dtype == PSC_BF16;
+    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    if (fast) {
+        const int words_per_block = (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
+                                                                  : ApplyGeom<false>::kWordsPerWave);
+        dim3 grid((W + words_per_block - 1) / words_per_block, B);
+        if (bf16)
+            hipLaunchKernelGGL(decode_fast_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
+                               D, W, out_bitmask, err, reinterpret_cast<uint4 *>(logits));
+        else
+            hipLaunchKernelGGL(decode_fast_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks,
+                               h->mask_stride, D, W, out_bitmask, err, reinterpret_cast<uint4 *>(logits));
+    } else {
+        dim3 grid((W + kGenWords - 1) / kGenWords, B);
+        if (bf16)
+            hipLaunchKernelGGL(decode_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride, D,
+                               V, W, out_bitmask, err, logits);
+        else
+            hipLaunchKernelGGL(decode_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
+                               h->mask_stride, D, V, W, out_bitmask, err, logits);
+    }
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }
 
 extern "C" psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask, int32_t B, int32_t V,

@@ -22,7 +22,8 @@ _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
             "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
             "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_compute_and_argmax",
-            "psc_compute_and_argmax_dense", "psc_compute_classes", "psc_compute_classes_dense", "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
+            "psc_compute_and_argmax_dense", "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step",
+            "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
             "psc_free", "psc_last_error"]
 
 
@@ -85,6 +86,7 @@ def lib() -> C.CDLL:
         L.psc_compute_and_argmax_dense.argtypes = [P, P, I32, P, P, I32, P, C.c_int, I32, P, P]
         L.psc_compute_classes.argtypes = [P, P, P, P, I32, P, P]
         L.psc_compute_classes_dense.argtypes = [P, P, I32, P, P, I32, P, P]
+        L.psc_decode_step.argtypes = [P, P, P, P, P, P, P, I32, I32, P, P, P, P, C.c_int, I32, P]
         L.psc_save.argtypes = [P, C.c_char_p]
         L.psc_load.argtypes = [C.c_char_p, C.POINTER(P)]
         L.psc_state_reset.argtypes = [P, P, I32, P, P, I32, P]
@@ -100,7 +102,7 @@ def lib() -> C.CDLL:
         for name in ("psc_build", "psc_info", "psc_bind_device", "psc_compute_masks", "psc_apply_mask",
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
                      "psc_compute_and_apply_dense", "psc_compute_and_argmax", "psc_compute_and_argmax_dense",
-                     "psc_compute_classes", "psc_compute_classes_dense", "psc_save", "psc_load", "psc_device_error_count",
+                     "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step", "psc_save", "psc_load", "psc_device_error_count",
                      "psc_classify_host", "psc_class_mask_host"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -376,6 +378,30 @@ class DecodeStates:
                                                   logits.data_ptr(), dt, self.clf.V, out.data_ptr(),
                                                   _stream_ptr(stream)))
         return out
+
+    def decode_step(self, tokens, logits, out=None, stream=None):
+        """psc_decode_step: advance by `tokens` (int32 [B], < 0 = skip), then
+        mask `logits` [B, V] for the new states in place, in one launch.  The
+        new states go to a second set of buffers, which then become this
+        object's; returns the status tensor (ADV_*)."""
+        import torch
+        assert tokens.is_cuda and tokens.dtype == torch.int32 and tokens.numel() == self.B
+        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
+        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        if getattr(self, "_spare", None) is None:
+            self._spare = (torch.empty_like(self.stacks), torch.empty_like(self.lens), torch.empty_like(self.qs))
+        so, lo, qo = self._spare
+        out_ptr = None
+        if out is not None:
+            assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
+            out_ptr = out.data_ptr()
+        _check(lib().psc_decode_step(self.clf._h, self.stacks.data_ptr(), self.lens.data_ptr(), self.qs.data_ptr(),
+                                     so.data_ptr(), lo.data_ptr(), qo.data_ptr(), self.cap, self.B,
+                                     tokens.data_ptr(), self.status.data_ptr(), out_ptr, logits.data_ptr(), dt,
+                                     self.clf.V, _stream_ptr(stream)))
+        self._spare = (self.stacks, self.lens, self.qs)
+        self.stacks, self.lens, self.qs = so, lo, qo
+        return self.status
 
     def host_states(self):
         """The states as host (q, stack) pairs (synchronises)."""

@@ -206,3 +206,64 @@ def test_advance_long_production(fillers):
         if k % 50 == 0:
             assert np.array_equal(ds.compute_masks().cpu().numpy().view(np.uint32), orc.masks(want)), k
     assert st[0] == psc.ADV_EOS
+
+
+@pytest.mark.parametrize("name,B,steps,dtype", [("json", 16, 30, None), ("schema", 64, 25, None),
+                                                ("pylike", 32, 20, None), ("arithmetic", 24, 30, None),
+                                                ("schema", 9, 12, torch.float32)])
+def test_decode_step_equals_advance_then_step(built, name, B, steps, dtype):
+    """psc_decode_step (one launch) against psc_advance followed by
+    psc_compute_and_apply_dense on a copy of the same states: status, new
+    states, bitmask and masked logits identical at every step; tokens mix
+    allowed ones, EOS, skips and (every fifth step) random ones."""
+    wl, clf, orc = built(name)
+    rng = np.random.default_rng(7)
+    cap = 512
+    a = DecodeStates(clf, B, cap, DEV)
+    r = DecodeStates(clf, B, cap, DEV)
+    clf.error_count(reset=True)
+    eos = wl.vocab.eos_id
+    for k in range(steps):
+        bm = r.compute_masks().cpu().numpy().view(np.uint32)
+        toks = np.full(B, -1, np.int32)
+        for b in range(B):
+            allowed = np.nonzero(np.unpackbits(bm[b].astype("<u4").view(np.uint8), bitorder="little")[:wl.V])[0]
+            allowed = allowed[allowed != eos]
+            if k % 5 == 4 or allowed.size == 0:
+                toks[b] = rng.integers(0, wl.V)
+            elif b % 7 == 3:
+                toks[b] = eos if k % 2 else -1
+            else:
+                toks[b] = rng.choice(allowed)
+        t = torch.from_numpy(toks).to(DEV)
+        logits = wl.logits(k, B=B)
+        if dtype is not None:
+            logits = logits.to(dtype)
+        l1, l2 = logits.to(DEV), logits.to(DEV)
+        o1 = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
+        o2 = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
+        s1 = a.decode_step(t, l1, out=o1).clone()
+        s2 = r.advance(t).clone()
+        r.compute_and_apply(l2, out=o2)
+        torch.cuda.synchronize()
+        assert torch.equal(s1, s2), (k, s1.cpu().numpy(), s2.cpu().numpy())
+        assert _same_states(a.host_states(), r.host_states()) < 0, k
+        assert torch.equal(o1, o2), k
+        assert torch.equal(l1.view(torch.int16 if l1.dtype == torch.bfloat16 else torch.int32).cpu(),
+                           l2.view(torch.int16 if l2.dtype == torch.bfloat16 else torch.int32).cpu()), k
+        if k % 8 == 0:
+            assert np.array_equal(o1.cpu().numpy().view(np.uint32), orc.masks(a.host_states())), k
+
+
+def test_decode_step_rejects_overlapping_states(built):
+    wl, clf, _ = built("arithmetic")
+    ds = DecodeStates(clf, 4, 16, DEV)
+    t = torch.zeros(4, dtype=torch.int32, device=DEV)
+    logits = torch.zeros((4, wl.V), dtype=torch.float32, device=DEV)
+    with pytest.raises(psc.PscError):
+        psc.lib()  # loaded
+        _check = psc._check
+        _check(psc.lib().psc_decode_step(clf._h, ds.stacks.data_ptr(), ds.lens.data_ptr(), ds.qs.data_ptr(),
+                                         ds.stacks.data_ptr(), ds.lens.data_ptr(), ds.qs.data_ptr(), 16, 4,
+                                         t.data_ptr(), ds.status.data_ptr(), None, logits.data_ptr(),
+                                         psc.PSC_F32, wl.V, None))
