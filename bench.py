@@ -217,24 +217,32 @@ def main():
         t_upload = loop(upload, 1000)
         t_upload_step = loop(upload_step, 1000)
 
-        # the timed step captured in a HIP graph: G steps (rotating inputs
-        # and logits as above) per graph, replayed back to back
-        G = 100
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            for i in range(G):
-                step(i)
-        graph.replay()
-        torch.cuda.synchronize()
-        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        reps = max(1, min(args.steps, 2000) // G)
-        for _ in range(reps):
+        def graph_loop(fn, G=100, reps=10):
+            """G calls captured in a HIP graph (rotating inputs and logits as
+            above), replayed back to back: the GPU-side time per call, free
+            of the host's per-call cost."""
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                for i in range(G):
+                    fn(i)
             graph.replay()
-        z.record(stream)
-        torch.cuda.synchronize()
-        t_graph = a.elapsed_time(z) / (reps * G) * 1e3
-        del graph
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                graph.replay()
+            z.record(stream)
+            torch.cuda.synchronize()
+            del graph
+            return a.elapsed_time(z) / (reps * G) * 1e3
+
+        t_graph = graph_loop(step, reps=max(1, min(args.steps, 2000) // 100))
+        t_other_graph = graph_loop(other)
+        t_compute_graph = graph_loop(only_compute)
+        for i in range(n_bm):
+            only_compute(i)
+        t_apply_graph = graph_loop(only_apply)
+        t_argmax_graph = graph_loop(argmax_step)
 
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
         # advanced by one token each (psc_advance), then the single-launch
@@ -333,9 +341,12 @@ def main():
             "logits_pool_buffers": n_pool, "warm_cache": bool(args.warm_cache),
         },
         "step_mode": args.mode,
-        "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3)},
+        "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3),
+                               ("two_launch" if args.mode == "fused" else "fused") + "_graph":
+                                   round(t_other_graph, 3)},
         "decode_step_us": decode,
         "argmax_step_us": round(t_argmax, 3),
+        "argmax_step_graph_us": round(t_argmax_graph, 3),
         "walk_us": {"graph_replayed": round(t_walk, 3), "eager": round(t_walk_eager, 3),
                     "call": "psc_compute_classes (the walk alone, class ids out)"},
         "stack_depth": {"mean": round(float(np.mean(depth_hist)), 2),
@@ -347,7 +358,9 @@ def main():
                                 "bench stream before the step; PCIe-inclusive, not the headline"},
         "graph_step_us": round(t_graph, 3),
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
-                       "apply_mask_solo_gbs": round(achieved_apply, 1)},
+                       "apply_mask_solo_gbs": round(achieved_apply, 1),
+                       "compute_masks_solo_graph": round(t_compute_graph, 3),
+                       "apply_mask_solo_graph": round(t_apply_graph, 3)},
         "bytes_per_step": {"algorithmic": round(bytes_step), "fused": round(bytes_fused),
                            "two_launch": round(bytes_two_launch),
                            "one_pass_read_write_model": round(one_pass_model)},
