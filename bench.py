@@ -244,6 +244,20 @@ def main():
         t_apply_graph = graph_loop(only_apply)
         t_argmax_graph = graph_loop(argmax_step)
 
+        # what plain streaming kernels of the same size achieve on this GPU
+        # (torch's own fill and copy of one logits tensor, graph-replayed):
+        # the practical ceiling for a launch that touches this many bytes
+        def fill(i):
+            pool[i % n_pool].fill_(float("-inf"))
+
+        def copy(i):
+            pool[i % n_pool].copy_(pool[(i + 7) % n_pool])
+
+        # (after every timing of the mask kernels: the logits values do not
+        # affect the kernels' work, but the pool is overwritten from here on)
+        t_fill = graph_loop(fill)
+        t_copy = graph_loop(copy)
+
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
         # advanced by one token each (psc_advance), then the single-launch
         # step on them (psc_compute_and_apply_dense)
@@ -365,6 +379,11 @@ def main():
                            "two_launch": round(bytes_two_launch),
                            "one_pass_read_write_model": round(one_pass_model)},
         "roofline": roofline,
+        "reference_kernels_us": {
+            "torch_fill_logits": round(t_fill, 3), "torch_copy_logits": round(t_copy, 3),
+            "fill_gbs": round(B * V * s_logit / (t_fill * 1e-6) / 1e9, 1),
+            "copy_gbs": round(2 * B * V * s_logit / (t_copy * 1e-6) / 1e9, 1),
+            "note": "torch's fill_ and copy_ of one [B, V] logits tensor, 100 per HIP graph, replayed"},
         "cpu_baseline": cpu,
         "build": {k: info[k] for k in ("dfa_states_built", "dfa_states", "n_classes", "table_bytes",
                                         "mask_table_bytes", "build_seconds", "dfa_rows", "dense_rows",
