@@ -452,7 +452,7 @@ def decode_steps(wl, clf, B, pool, bms, stream, dev, max_steps):
     check()
     t_adv = run("advance")
     check()
-    return {"advance_and_fused_step": round(t_both, 3), "decode_step_one_launch": round(t_one, 3),
+    return {"advance_and_fused_step": round(t_both, 3), "psc_decode_step": round(t_one, 3),
             "advance": round(t_adv, 3), "tokens_per_sequence": n, "cap": cap, "states_checked": True}
 
 

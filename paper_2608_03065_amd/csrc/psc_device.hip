@@ -812,6 +812,30 @@ __device__ __forceinline__ int decode_block_class(const int32_t *__restrict__ ta
     return s_cls;
 }
 
+// psc_decode_step's first launch when its grid would not fit on the GPU at
+// once: one wavefront per sequence advances it and writes the new state
+// (the second launch is the fused step on the new states).
+__global__ void __launch_bounds__(kWave)
+advance_copy_kernel(DecodeArgs D) {
+    __shared__ int32_t s_ov[kOverlay];
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int cap = D.cap;
+    const int len = D.lens_in[b], q_in = D.qs_in[b];
+    const int32_t *st = D.stacks_in + (int64_t)b * cap;
+    int ptr, ov, q;
+    const int res = advance_core(D.T, s_ov, st, len, q_in, D.tokens[b], cap, lane, ptr, ov, q);
+    int32_t *dst = D.stacks_out + (int64_t)b * cap;
+    const int keep = res == PSC_ADV_OK ? ptr : min(max(len, 0), cap);
+    for (int k = lane; k < keep; k += kWave) dst[k] = st[k];
+    for (int k = lane; k < ov; k += kWave) dst[ptr + k] = s_ov[k];
+    if (lane == 0) {
+        D.lens_out[b] = res == PSC_ADV_OK ? ptr + ov : len;
+        D.qs_out[b] = q;
+        D.status[b] = res;
+    }
+}
+
 template <bool kBf16>
 __global__ void __launch_bounds__(kFusedBlock)
 decode_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
@@ -1022,6 +1046,17 @@ AdvTables adv_tables(const psc_handle *h) {
                      h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0};
 }
 
+// Workgroups of 256 threads that fit on the current GPU at once: 8 per
+// compute unit (4 SIMDs x 8 wavefronts; the fused kernels' registers allow
+// it), from the device's compute-unit count.
+int64_t resident_blocks() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    return (int64_t)cus * 8;
+}
+
 bool ranges_overlap(const void *a, const void *b, size_t n) {
     const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
     return x < y + n && y < x + n;
@@ -1210,6 +1245,20 @@ extern "C" psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks
     const int32_t W = h->W;
     const bool bf16 = dtype == PSC_BF16;
     const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    // When the fused grid does not fit on the GPU at once, workgroups that
+    // start late would repeat the advance after the early ones finished:
+    // then the advance runs once per sequence in a launch of its own and the
+    // fused step follows on the new states (same results).
+    const int words_per_block = !fast ? kGenWords
+                                      : (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
+                                                                      : ApplyGeom<false>::kWordsPerWave);
+    const int64_t n_blocks = (int64_t)((W + words_per_block - 1) / words_per_block) * B;
+    if (n_blocks > resident_blocks()) {
+        hipLaunchKernelGGL(advance_copy_kernel, dim3(B), dim3(kWave), 0, s, D);
+        hipError_t e0 = hipGetLastError();
+        if (e0 != hipSuccess) return device_fail(what, e0);
+        return launch_fused(h, stacks_out, cap, lens_out, qs_out, B, out_bitmask, logits, dtype, V, stream, what);
+    }
     if (fast) {
         const int words_per_block = (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
                                                                   : ApplyGeom<false>::kWordsPerWave);

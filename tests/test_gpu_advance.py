@@ -210,12 +210,13 @@ def test_advance_long_production(fillers):
 
 @pytest.mark.parametrize("name,B,steps,dtype", [("json", 16, 30, None), ("schema", 64, 25, None),
                                                 ("pylike", 32, 20, None), ("arithmetic", 24, 30, None),
-                                                ("schema", 9, 12, torch.float32)])
+                                                ("schema", 9, 12, torch.float32), ("stress", 256, 8, None)])
 def test_decode_step_equals_advance_then_step(built, name, B, steps, dtype):
     """psc_decode_step (one launch) against psc_advance followed by
     psc_compute_and_apply_dense on a copy of the same states: status, new
     states, bitmask and masked logits identical at every step; tokens mix
-    allowed ones, EOS, skips and (every fifth step) random ones."""
+    allowed ones, EOS, skips and (every fifth step) random ones.  The stress
+    shape (8,192 workgroups) takes the two-launch form of the call."""
     wl, clf, orc = built(name)
     rng = np.random.default_rng(7)
     cap = 512
