@@ -310,7 +310,8 @@ psc_status psc_compute_and_apply_dense(const psc_handle *h, const int32_t *stack
                                        void *stream);
 
 /*
- * One whole decoding step of Algorithm 2 in one launch, on device-resident
+ * One whole decoding step of Algorithm 2 in one launch (two when the batch
+ * is too large for all its workgroups to run at once), on device-resident
  * states: the lexing and parsing steps (psc_advance by tokens[b]), then the
  * classification and mask steps of the new state, applied to the logits
  * (psc_compute_and_apply_dense).  The results (new states, status, bitmask,
