@@ -1,10 +1,12 @@
 // Device side of the mask library (gfx950): table binding, the classifier
-// walk + mask gather (Algorithm 2, classification and mask steps), and the
-// in-place bitmask -> logits application.
+// walk + mask gather (Algorithm 2, classification and mask steps), the
+// in-place bitmask -> logits application, the fused single-launch step, the
+// masked argmax, and the lexing and parsing steps on device-resident prefix
+// states (the advance, and the whole decoding step in one launch).
 //
 // Nothing here is a dense contraction, so no matrix cores are used; the walk
-// is a chain of dependent table loads (latency-bound) and the application is
-// a pure HBM stream.
+// and the advance are chains of dependent table loads (latency-bound) and
+// the application is a pure HBM stream.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
