@@ -117,3 +117,30 @@ def test_device_masks_match_oracle_on_random_grammars(cases):
         assert clf.error_count() == 0
         del torch
         torch = pytest.importorskip("torch")
+
+
+@pytest.mark.gpu
+def test_device_advance_matches_oracle_on_random_grammars(cases):
+    """psc_advance and psc_decode_step on the same states with random
+    tokens (allowed or not, EOS included) against the oracle's advance."""
+    torch = pytest.importorskip("torch")
+    from paper_2608_03065_amd import psc
+    from paper_2608_03065_amd.psc import DecodeStates
+    cap = 64
+    for seed, g, vocab, clf, orc, states in cases:
+        clf.bind("cuda:0")
+        sel = [states[i] for i in range(0, len(states), max(1, len(states) // 64))][:64]
+        rng = np.random.default_rng(seed)
+        toks = rng.integers(0, len(vocab.tokens), len(sel)).astype(np.int32)
+        ds = DecodeStates(clf, len(sel), cap, "cuda:0").load(sel)
+        st = ds.advance(torch.from_numpy(toks).to("cuda:0")).cpu().numpy()
+        dd = DecodeStates(clf, len(sel), cap, "cuda:0").load(sel)
+        logits = torch.zeros((len(sel), len(vocab.tokens)), dtype=torch.float32, device="cuda:0")
+        st2 = dd.decode_step(torch.from_numpy(toks).to("cuda:0"), logits).cpu().numpy()
+        got, got2 = ds.host_states(), dd.host_states()
+        for b, (s0, t) in enumerate(zip(sel, toks)):
+            code, new = orc.advance(s0, int(t), cap)
+            want = new if code == Oracle.ADVANCED else s0
+            assert st[b] == code and st2[b] == code, (seed, b)
+            for q, a in (got[b], got2[b]):
+                assert q == want[0] and np.array_equal(a, want[1]), (seed, b)
