@@ -918,7 +918,7 @@ size_t psc_handle::device_bytes_needed() const {
     auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
     return kTableOff + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
            up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes +
-           up((size_t)n_lr * adv.n_term * sizeof(int32_t));
+           up((size_t)n_lr * adv.n_term * sizeof(int32_t)) + up(psc::goto_closure_bytes(*this));
 }
 
 namespace psc {
@@ -937,6 +937,39 @@ bool packed_action(const psc_handle &h, std::vector<int32_t> &out) {
     }
     out.swap(v);
     return true;
+}
+
+size_t goto_closure_bytes(const psc_handle &h) {
+    const size_t n = (size_t)h.n_lr * h.adv.n_nt * h.adv.n_term * sizeof(int32_t);
+    return n <= kClosureMaxBytes ? n : 0;
+}
+
+void goto_closure(const psc_handle &h, std::vector<int32_t> &out) {
+    out.clear();
+    if (!goto_closure_bytes(h)) return;
+    const AdvanceLayout &L = h.adv;
+    const int32_t *act = h.gram.data() + L.action, *go = h.gram.data() + L.go,
+                  *lhs = h.gram.data() + L.prod_lhs, *len = h.gram.data() + L.prod_len;
+    const int64_t nt = L.n_nt, nT = L.n_term;
+    out.assign((size_t)h.n_lr * nt * nT, -1);
+    for (int64_t s = 0; s < h.n_lr; s++)
+        for (int64_t A = 0; A < nt; A++) {
+            const int32_t g0 = go[s * nt + A];
+            int32_t *row = out.data() + (s * nt + A) * nT;
+            if (g0 < 0) continue;
+            for (int64_t t = 0; t < nT; t++) {
+                int32_t x = g0;
+                int64_t steps = 0;
+                for (;;) {
+                    const int32_t a = act[(int64_t)x * nT + t];
+                    if ((a & 3) != 2 || len[a >> 2] != 1) break;
+                    if (++steps > nt) { x = g0; break; }      // a cycle of unit productions: not skipped
+                    x = go[s * nt + lhs[a >> 2]];
+                    if (x < 0) break;
+                }
+                row[t] = x;
+            }
+        }
 }
 }  // namespace psc
 

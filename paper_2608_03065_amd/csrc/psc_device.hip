@@ -600,6 +600,7 @@ struct AdvTables {
     const uint8_t *bytes;
     int32_t n_lex, n_lr, n_term, n_nt, end_term, eos, V;
     int32_t packed;    // action holds packed reductions (kind | len << 2 | lhs << 10)
+    const int32_t *closure;   // GOTO with the following unit reductions done, or null
 };
 
 constexpr int kOverlay = 192;          // states one token may push above what it keeps
@@ -668,7 +669,11 @@ __device__ __forceinline__ int advance_core(const AdvTables &T, int32_t *s_ov, c
             reload();
             const int32_t s1 = cur;
             if (s1 < 0 || s1 >= T.n_lr) return PSC_ADV_BAD_INPUT;
-            const int32_t g = T.go[(int64_t)s1 * T.n_nt + lhs];
+            // with the closure, the unit reductions the lookahead selects
+            // next are done here too (each would pop the state just pushed
+            // and push a GOTO from s1): the stack ends the same
+            const int32_t g = T.closure ? T.closure[((int64_t)s1 * T.n_nt + lhs) * T.n_term + t]
+                                        : T.go[(int64_t)s1 * T.n_nt + lhs];
             if (g < 0) return PSC_ADV_REJECTED;
             if (!push(g)) return PSC_ADV_OVERFLOW;
         }
@@ -1045,7 +1050,8 @@ AdvTables adv_tables(const psc_handle *h) {
     const int32_t *action = h->action_packed ? reinterpret_cast<const int32_t *>(base + h->packed_off) : g + L.action;
     return AdvTables{g + L.lex_next, g + L.lex_accept, g + L.ignored, action, g + L.go, g + L.prod_lhs,
                      g + L.prod_len, g + L.tok_off, reinterpret_cast<const uint8_t *>(base + h->vbytes_off),
-                     h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0};
+                     h->n_lex, h->n_lr, L.n_term, L.n_nt, L.end_term, L.eos, h->V, h->action_packed ? 1 : 0,
+                     h->has_closure ? reinterpret_cast<const int32_t *>(base + h->closure_off) : nullptr};
 }
 
 // Workgroups of 256 threads that fit on the current GPU at once: 8 per
@@ -1086,6 +1092,9 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     const size_t packed_off = argmax_off + kArgmaxBytes;
     std::vector<int32_t> packed;
     const bool is_packed = packed_action(*h, packed);
+    const size_t closure_off = packed_off + up((size_t)h->n_lr * h->adv.n_term * sizeof(int32_t));
+    std::vector<int32_t> closure;
+    goto_closure(*h, closure);
     hipError_t e = hipMemsetAsync(base, 0, kTableOff, s);
     if (e == hipSuccess) e = hipMemsetAsync(base + argmax_off, 0, kArgmaxBytes, s);
     if (e == hipSuccess)
@@ -1102,6 +1111,9 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     if (e == hipSuccess && is_packed)
         e = hipMemcpyAsync(base + packed_off, packed.data(), packed.size() * sizeof(int32_t), hipMemcpyHostToDevice,
                            s);
+    if (e == hipSuccess && !closure.empty())
+        e = hipMemcpyAsync(base + closure_off, closure.data(), closure.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return device_fail("psc_bind_device", e);
     h->dev_base = dev_buf;
@@ -1112,6 +1124,8 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     h->argmax_off = argmax_off;
     h->packed_off = packed_off;
     h->action_packed = is_packed;
+    h->closure_off = closure_off;
+    h->has_closure = !closure.empty();
     return PSC_OK;
 }
 

@@ -77,6 +77,7 @@ struct AdvanceLayout {
 //   [vbytes_off, ...)          uint8 vocabulary bytes
 //   [argmax_off, ...)          uint64 [65536] masked-argmax slots (zero between calls)
 //   [packed_off, ...)          int32 ACTION with packed reductions (packed_action)
+//   [closure_off, ...)         int32 unit-reduction closure of GOTO (goto_closure), when it fits
 constexpr size_t kTableOff = 256;
 constexpr size_t kArgmaxBytes = 65536 * sizeof(unsigned long long);
 
@@ -94,8 +95,9 @@ struct psc_handle {
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
-    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0;
+    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0, closure_off = 0;
     bool action_packed = false;    // the device ACTION copy carries each reduction's length and lhs
+    bool has_closure = false;      // the device holds the unit-reduction closure of GOTO
     size_t device_bytes_needed() const;
 };
 
@@ -106,6 +108,17 @@ void set_error(const std::string &msg);
 // reduction needs no second table read.  Returns false (and leaves `out`
 // empty) when some production does not fit (length > 255 or lhs >= 2^21).
 bool packed_action(const psc_handle &h, std::vector<int32_t> &out);
+// GOTO followed by the unit reductions the lookahead then selects:
+// closure[(s * n_nt + A) * n_term + t] is the state on top after a reduction
+// to A returns to state s with lookahead t, GOTO[s][A] pushed and every
+// following reduction by a one-symbol production done (each pops the state
+// just pushed and pushes GOTO[s][B], so s stays below); -1 where a GOTO in
+// that run is missing.  A run longer than n_nt (a cycle of unit
+// productions) is left undone: the entry is GOTO[s][A].  Only built when it
+// takes at most kClosureMaxBytes.
+constexpr size_t kClosureMaxBytes = 64u << 20;
+size_t goto_closure_bytes(const psc_handle &h);
+void goto_closure(const psc_handle &h, std::vector<int32_t> &out);
 // The input checks of psc_build (ids in range, spellings), for loaded tables.
 psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg);
 }
