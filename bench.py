@@ -456,11 +456,23 @@ def decode_steps(wl, clf, B, pool, bms, stream, dev, max_steps):
             "advance": round(t_adv, 3), "tokens_per_sequence": n, "cap": cap, "states_checked": True}
 
 
+def device_code_hash() -> str:
+    """sha256 (first 16 hex digits) of the device source with its comments
+    and blank space removed: a change of the code, not of its comments,
+    makes the stored counter readings stale."""
+    import hashlib
+    import re
+    src = open(os.path.join(ROOT, "paper_2608_03065_amd", "csrc", "psc_device.hip")).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    src = " ".join(src.split())
+    return hashlib.sha256(src.encode()).hexdigest()[:16]
+
+
 def measured_traffic(workload: str, kernel: str):
     """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
     None when there is none for this workload or the kernel source changed
     since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"{workload}_c3_pmc_traffic.md" if workload == "schema" else
                         f"{workload}_pmc_traffic.md")
     if not os.path.exists(path):
@@ -469,8 +481,7 @@ def measured_traffic(workload: str, kernel: str):
     for line in open(path):
         if line.startswith("traffic_json: "):
             meta = json.loads(line[len("traffic_json: "):])
-    src = os.path.join(ROOT, "paper_2608_03065_amd", "csrc", "psc_device.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = device_code_hash()
     if not meta or meta.get("source_sha256_16") != h or kernel not in meta.get("kernels", {}):
         return None
     return meta["kernels"][kernel]["hbm_bytes"]

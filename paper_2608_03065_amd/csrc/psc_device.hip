@@ -197,11 +197,10 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
     }
 }
 
-// Wavefront 0 of the workgroup walks sequence b; the class (or -1) is
-// published to the whole workgroup through LDS.  Slice 0 of each sequence
-// counts rejected inputs.  Round trip 1 fetches lens[b], qs[b] and, for
-// ragged stacks (stride 0), the lengths before b (the stack's offset); with
-// stride > 0 stack b starts at b * stride and holds at most stride symbols.
+// One wavefront walks sequence b and returns its class, or -1 for an input
+// out of range.  Round trip 1 fetches lens[b], qs[b] and, for ragged stacks
+// (stride 0), the lengths before b (the stack's offset); with stride > 0
+// stack b starts at b * stride and holds at most stride symbols.
 __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                           const int32_t *__restrict__ stacks, int32_t stride,
                                           const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
@@ -220,6 +219,9 @@ __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int
     return -1;
 }
 
+// Wavefront 0 of the workgroup walks sequence b; the class (or -1) is
+// published to the whole workgroup through LDS.  Slice 0 of each sequence
+// counts rejected inputs.
 __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                            const int32_t *__restrict__ stacks, int32_t stride,
                                            const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
