@@ -234,11 +234,11 @@ psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, con
  * every number, -0 equals +0, and a row with no allowed token (or a rejected
  * input, as in psc_compute_masks) gives -1.  The logits (device, contiguous
  * [B][V] of `dtype`, V = the vocabulary size) are only read, and only the
- * 16-byte groups that hold an allowed token.  Two kernel launches; the
- * workgroups of a sequence combine their results in a per-sequence slot of
- * the bound device buffer, which each call leaves at zero, so argmax calls
- * on one handle must not overlap in time (one stream, or synchronised
- * streams).  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND, PSC_E_DEVICE.
+ * 16-byte groups that hold an allowed token.  One kernel launch; the
+ * workgroups of a sequence combine their results in a per-sequence slot and
+ * arrival counter of the bound device buffer, which each call leaves at
+ * zero, so argmax calls on one handle must not overlap in time (one stream,
+ * or synchronised streams).  B <= 65535.  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND, PSC_E_DEVICE.
  */
 psc_status psc_compute_and_argmax(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                   const int32_t *lexer_states, int32_t B, const void *logits, psc_dtype dtype,

@@ -494,13 +494,19 @@ fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restri
 // Greedy decoding folded into the mask step: out[b] = the allowed token with
 // the largest logit (ties to the lowest id; NaN above everything; -1 if no
 // token is allowed).  The logits are only read, and only the 16-byte vectors
-// holding at least one allowed token.  Two launches: argmax_partial_kernel
-// has the fused step's workgroups (one per sequence and slice of the row);
-// each folds its best (value, id) key into the sequence's slot with a 64-bit
-// atomic max, and argmax_finish_kernel, ordered after it by the launch
-// boundary, turns every slot into a token and clears it for the next call.
-// (A single launch would need device-scope fences between the workgroups of
-// a sequence, and those write back a whole L2 on this GPU.)
+// holding at least one allowed token.  One launch with the fused step's
+// workgroups (one per sequence and slice of the row): each folds its best
+// (value, id) key into the sequence's slot with a 64-bit atomic max, then
+// counts itself in the sequence's arrival counter; the workgroup that
+// arrives last takes the slot (an atomic exchange with zero), clears the
+// counter and writes the token.  Slot and counter are touched only by
+// device-scope atomics, which every XCD performs at the same point, and a
+// workgroup's counter increment is issued only after its max has returned,
+// so the last arrival sees every max without a fence (a device-scope release
+// would write back a whole L2 on this GPU).  Both are zero between calls.
+// Each sequence's slot and counter share a 128-byte record of their own:
+// with 32 counters packed in a cache line, the atomics queued on that line
+// cost 1.5 us per C3 step.
 
 // An order-preserving key: larger float, larger key; NaN above +inf; -0 = +0.
 __device__ __forceinline__ uint32_t order_key(uint32_t u) {
@@ -523,7 +529,7 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
                       int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
                       const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
                       uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
-                      unsigned long long *__restrict__ slots) {
+                      unsigned long long *__restrict__ records, int32_t *__restrict__ out_tokens) {
     using G = ApplyGeom<kBf16>;
     __shared__ unsigned long long s_best[kFusedBlock / kWave];
     const int b = blockIdx.y;
@@ -580,17 +586,18 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
     __syncthreads();
     if (threadIdx.x == 0) {
         for (int k = 1; k < kFusedBlock / kWave; k++) best = umax64(best, s_best[k]);
-        if (best) atomicMax(slots + b, best);
+        unsigned long long *slot = records + (size_t)b * kArgmaxRecordWords;
+        uint32_t *arrivals = reinterpret_cast<uint32_t *>(slot + 1);
+        const unsigned long long seen = __hip_atomic_fetch_max(slot, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // the max has been performed once its old value is back
+        asm volatile("s_waitcnt vmcnt(0)" ::"v"((uint32_t)seen) : "memory");
+        const uint32_t arrived = __hip_atomic_fetch_add(arrivals, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (arrived == gridDim.x - 1) {
+            const unsigned long long k = __hip_atomic_exchange(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_exchange(arrivals, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            out_tokens[b] = k ? (int32_t)(0xFFFFFFFFu - (uint32_t)k) : -1;
+        }
     }
-}
-
-__global__ void __launch_bounds__(kBlock)
-argmax_finish_kernel(unsigned long long *__restrict__ slots, int32_t B, int32_t *__restrict__ out) {
-    const int b = blockIdx.x * kBlock + threadIdx.x;
-    if (b >= B) return;
-    const unsigned long long k = slots[b];
-    slots[b] = 0;
-    out[b] = k ? (int32_t)(0xFFFFFFFFu - (uint32_t)k) : -1;
 }
 
 // ---------------------------------------------------------------- advance
@@ -1014,19 +1021,15 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
                                       : (kFusedBlock / kWave) * (dtype == PSC_BF16 ? ApplyGeom<true>::kWordsPerWave
                                                                                    : ApplyGeom<false>::kWordsPerWave);
     dim3 grid((W + words_per_block - 1) / words_per_block, B);
-    auto *slots = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
+    auto *records = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
     if (dtype == PSC_BF16)
         hipLaunchKernelGGL(argmax_partial_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                            h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
-                           slots);
+                           records, out_tokens);
     else
         hipLaunchKernelGGL(argmax_partial_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
                            h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
-                           slots);
-    hipError_t e0 = hipGetLastError();
-    if (e0 != hipSuccess) return device_fail(what, e0);
-    hipLaunchKernelGGL(argmax_finish_kernel, dim3((B + kBlock - 1) / kBlock), dim3(kBlock), 0, s, slots, B,
-                       out_tokens);
+                           records, out_tokens);
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }

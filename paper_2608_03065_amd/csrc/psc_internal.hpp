@@ -75,11 +75,14 @@ struct AdvanceLayout {
 //   [mask_off, ...)            uint32 masks [n_classes][mask_stride] (256-B aligned)
 //   [gram_off, ...)            int32 advance blob (AdvanceLayout)
 //   [vbytes_off, ...)          uint8 vocabulary bytes
-//   [argmax_off, ...)          uint64 [65536] masked-argmax slots (zero between calls)
+//   [argmax_off, ...)          masked argmax: [65536] records of 128 bytes, each a uint64
+//                              slot then a uint32 arrival counter (zero between calls)
 //   [packed_off, ...)          int32 ACTION with packed reductions (packed_action)
 //   [closure_off, ...)         int32 unit-reduction closure of GOTO (goto_closure), when it fits
 constexpr size_t kTableOff = 256;
-constexpr size_t kArgmaxBytes = 65536 * sizeof(unsigned long long);
+constexpr size_t kArgmaxSlots = 65536;
+constexpr size_t kArgmaxRecordWords = 16;   // uint64 words per record: one 128-byte cache line
+constexpr size_t kArgmaxBytes = kArgmaxSlots * kArgmaxRecordWords * sizeof(unsigned long long);
 
 }  // namespace psc
 

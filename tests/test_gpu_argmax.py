@@ -125,3 +125,53 @@ def test_greedy_decoding_on_device(built, name, B, steps):
         got = ds.host_states()
         for b in range(B):
             assert got[b][0] == host[b][0] and np.array_equal(got[b][1], host[b][1]), (k, b)
+
+
+def test_argmax_calls_in_a_row_leave_no_state(built):
+    """The per-sequence slots and arrival counters are cleared by each call:
+    a full batch, a smaller one, the general path and the full batch again,
+    back to back on one stream, each against the closed form."""
+    wl, clf, orc = built("schema")
+    cases = [(wl.states(40), 0), (wl.states(41)[:5], 0), (wl.states(42)[:9], 1), (wl.states(43), 0)]
+    launched = []
+    for k, (states, offset) in enumerate(cases):
+        logits = wl.logits(40 + k)[:len(states)].contiguous()
+        buf = torch.empty(offset + logits.numel(), dtype=logits.dtype, device=DEV)
+        dev = buf[offset:].view(logits.shape)
+        dev.copy_(logits.to(DEV))
+        stacks, lens, qs = pack_states(states, DEV)
+        launched.append((clf.compute_and_argmax(stacks, lens, qs, dev), logits, states, dev, stacks, lens, qs))
+    torch.cuda.synchronize()
+    for got, logits, states, *_ in launched:
+        assert np.array_equal(got.cpu().numpy(), _closed_form(logits, orc.masks(states), wl.V))
+
+
+def test_argmax_graph_replays(built):
+    """The masked argmax captured in a HIP graph: every replay, with new
+    logits written into the captured buffer and eager argmax calls between
+    the replays, gives the eager result."""
+    wl, clf, orc = built("json")
+    states = wl.states(20)
+    stacks, lens, qs = pack_states(states, DEV)
+    g_logits = wl.logits(0).to(DEV)
+    g_out = torch.full((len(states),), -7, dtype=torch.int32, device=DEV)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        clf.compute_and_argmax(stacks, lens, qs, g_logits, out=g_out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        clf.compute_and_argmax(stacks, lens, qs, g_logits, out=g_out)
+    want_bits = orc.masks(states)
+    for rep in range(4):
+        logits = wl.logits(100 + rep)
+        g_logits.copy_(logits.to(DEV))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        eager = clf.compute_and_argmax(stacks, lens, qs, logits.to(DEV))
+        torch.cuda.synchronize()
+        assert torch.equal(g_out, eager), rep
+        assert np.array_equal(g_out.cpu().numpy(), _closed_form(logits, want_bits, wl.V)), rep
