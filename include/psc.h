@@ -169,8 +169,13 @@ psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *st
  * determined, and copy that class's precomputed mask into
  * out_bitmask[b][0..W).
  *  stacks       device int32, the B stacks concatenated in batch order, each
- *               stored bottom -> top (LR start state first, top last).
- *  stack_lens   device int32 [B], each >= 1.
+ *               stored bottom -> top (LR start state first, top last); the
+ *               total may exceed 2^31 symbols.  Each sequence finds its
+ *               stack by summing the lengths before it (O(B) reads per
+ *               sequence): for large batches the dense layout below is
+ *               cheaper.
+ *  stack_lens   device int32 [B], each >= 1 (a negative length holds no
+ *               symbols of `stacks`).
  *  lexer_states device int32 [B].
  *  out_bitmask  device uint32 [B][W], W = ceil(V/32), fully written.
  * A sequence with an out-of-range lexer state or stack symbol, or a length

@@ -22,10 +22,31 @@ constexpr int kWave = 64;
 constexpr int kBlock = 256;          // 4 wavefronts
 constexpr int kCopyWordsPerBlock = 2048;
 
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-    return v;
+// v + v of another lane, moved by a DPP control (kCtrl) into the rows of
+// kRowMask (the other rows add zero); 64 bits as two 32-bit moves.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int64_t dpp_add(int64_t v) {
+    const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)((uint64_t)v >> 32);
+    const uint32_t tlo = (uint32_t)__builtin_amdgcn_update_dpp(0, lo, kCtrl, kRowMask, 0xF, false);
+    const uint32_t thi = (uint32_t)__builtin_amdgcn_update_dpp(0, hi, kCtrl, kRowMask, 0xF, false);
+    return v + (int64_t)(((uint64_t)thi << 32) | tlo);
+}
+
+// The sum of v over the 64 lanes of a full wavefront, uniform.  DPP moves
+// instead of LDS-crossbar shuffles: sums of quads (two quad permutes), of
+// 8- and 16-lane rows (half-row and row mirrors), then lane 15 of rows 0
+// and 2 broadcast into rows 1 and 3, and lane 31 into rows 2 and 3, leaving
+// the total in lane 63.
+__device__ __forceinline__ int64_t wave_sum(int64_t v) {
+    v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]
+    v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
+    v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+    v = dpp_add<0x140, 0xF>(v);   // row_mirror
+    v = dpp_add<0x142, 0xA>(v);   // row_bcast:15
+    v = dpp_add<0x143, 0xC>(v);   // row_bcast:31
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), 63);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -197,19 +218,45 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
     }
 }
 
+// The lengths of sequences i0 + k * kWave + lane, k < kN, loaded in one
+// round trip (every load issued before the first is used), negative ones as
+// zero, summed per lane.
+constexpr int kLensPerRound = 4;
+
+template <int kN>
+__device__ __forceinline__ int64_t lens_round(__amdgpu_buffer_rsrc_t rl, int i0, int lane) {
+    int v[kN];
+#pragma unroll
+    for (int k = 0; k < kN; k++)
+        v[k] = (int)__builtin_amdgcn_raw_buffer_load_b32(rl, (uint32_t)(i0 + k * kWave + lane) * 4u, 0, 0);
+    int64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < kN; k++) sum += max(v[k], 0);
+    return sum;
+}
+
 // One wavefront walks sequence b and returns its class, or -1 for an input
 // out of range.  Round trip 1 fetches lens[b], qs[b] and, for ragged stacks
-// (stride 0), the lengths before b (the stack's offset); with stride > 0
-// stack b starts at b * stride and holds at most stride symbols.
+// (stride 0), the lengths before b (more round trips past 64 sequences):
+// the stack's offset, summed in 64 bits
+// (the stacks may hold more than 2^31 symbols in all), a negative length
+// counting as zero; with stride > 0 stack b starts at b * stride and holds at
+// most stride symbols.
 __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                           const int32_t *__restrict__ stacks, int32_t stride,
                                           const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
                                           int b, int lane) {
     const int own = *((lane & 1) ? qs + b : lens + b);
-    int part = 0;
+    int64_t part = 0;
     if (stride == 0) {
-        part = lane < b ? lens[lane] : 0;
-        for (int i = lane + kWave; i < b; i += kWave) part += lens[i];
+        // a buffer resource over lens[0..b) turns the loads past b into
+        // zeros without a branch
+        const __amdgpu_buffer_rsrc_t rl = wave_rsrc(lens, (uint32_t)b * 4u);
+        if (b <= kWave) {
+            part = lens_round<1>(rl, 0, lane);
+        } else {
+            for (int i0 = 0; i0 < b; i0 += kLensPerRound * kWave) part += lens_round<kLensPerRound>(rl, i0, lane);
+        }
     }
     const int len = __builtin_amdgcn_readlane(own, 0);
     const int q = __builtin_amdgcn_readlane(own, 1);
@@ -613,7 +660,15 @@ struct AdvTables {
 };
 
 constexpr int kOverlay = 192;          // states one token may push above what it keeps
-constexpr int kFeedSteps = 1 << 16;    // bound on the LR steps of one terminal
+// Bound on the LR steps that feeding one terminal may take.  A parse of any
+// stack ends long before it: every reduction that does not shrink the stack
+// is a unit or an empty one, at most one per nonterminal before the stack
+// shrinks or grows (an LR grammar has no derivation cycles), and growth
+// stops at the capacity.  The bound only keeps a wave from spinning on
+// tables or stacks that are not what they should be.
+__device__ __forceinline__ int64_t feed_step_bound(int32_t n_nt, int len, int cap) {
+    return (int64_t)(n_nt + 2) * (4 * (int64_t)len + 4 * (int64_t)cap + 8) + 65536;
+}
 
 // One wavefront advances one sequence by one token.  Everything it computes
 // is uniform across the wavefront (the sequence is the workgroup's), so the
@@ -651,8 +706,9 @@ __device__ __forceinline__ int advance_core(const AdvTables &T, int32_t *s_ov, c
     };
     // states come from the tables (validated when built) or, below the
     // overlay, from the caller's stack, which is checked before each use
+    const int64_t max_steps = feed_step_bound(T.n_nt, len, cap);
     auto feed = [&](int32_t t) -> int {
-        for (int guard = 0; guard < kFeedSteps; guard++) {
+        for (int64_t guard = 0; guard < max_steps; guard++) {
             const int32_t s0 = cur;
             if (s0 < 0 || s0 >= T.n_lr) return PSC_ADV_BAD_INPUT;
             const int32_t a = T.action[(int64_t)s0 * T.n_term + t];
