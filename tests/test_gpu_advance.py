@@ -208,15 +208,18 @@ def test_advance_long_production(fillers):
     assert st[0] == psc.ADV_EOS
 
 
-@pytest.mark.parametrize("name,B,steps,dtype", [("json", 16, 30, None), ("schema", 64, 25, None),
-                                                ("pylike", 32, 20, None), ("arithmetic", 24, 30, None),
-                                                ("schema", 9, 12, torch.float32), ("stress", 256, 8, None)])
-def test_decode_step_equals_advance_then_step(built, name, B, steps, dtype):
+@pytest.mark.parametrize("name,B,steps,dtype,offset", [
+    ("json", 16, 30, None, 0), ("schema", 64, 25, None, 0), ("pylike", 32, 20, None, 0),
+    ("arithmetic", 24, 30, None, 0), ("schema", 9, 12, torch.float32, 0), ("stress", 256, 8, None, 0),
+    ("stress", 256, 4, None, 1), ("stress", 96, 4, torch.float32, 0)])
+def test_decode_step_equals_advance_then_step(built, name, B, steps, dtype, offset):
     """psc_decode_step (one launch) against psc_advance followed by
     psc_compute_and_apply_dense on a copy of the same states: status, new
     states, bitmask and masked logits identical at every step; tokens mix
     allowed ones, EOS, skips and (every fifth step) random ones.  The stress
-    shape (8,192 workgroups) takes the two-launch form of the call."""
+    shapes (more workgroups than fit on the GPU at once) take the two-launch
+    form of the call, on the fast path and, with misaligned logits, on the
+    general one."""
     wl, clf, orc = built(name)
     rng = np.random.default_rng(7)
     cap = 512
@@ -240,7 +243,10 @@ def test_decode_step_equals_advance_then_step(built, name, B, steps, dtype):
         logits = wl.logits(k, B=B)
         if dtype is not None:
             logits = logits.to(dtype)
-        l1, l2 = logits.to(DEV), logits.to(DEV)
+        buf = torch.empty(offset + logits.numel(), dtype=logits.dtype, device=DEV)
+        l1 = buf[offset:].view(logits.shape)
+        l1.copy_(logits.to(DEV))
+        l2 = logits.to(DEV)
         o1 = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
         o2 = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
         s1 = a.decode_step(t, l1, out=o1).clone()

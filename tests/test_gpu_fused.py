@@ -61,7 +61,9 @@ def test_fused_step_bit_exact(built, name, steps):
     ("json", torch.bfloat16, 0),         # V = 32000: fast path, the other dtype
     ("json", torch.float32, 1),          # misaligned logits: general path
     ("schema", torch.float32, 0),        # fast path, fp32
-    ("schema", torch.bfloat16, 3)])      # misaligned bf16: general path
+    ("schema", torch.bfloat16, 3),       # misaligned bf16: general path
+    ("stress", torch.float32, 0),        # fast path, fp32, 16,384 workgroups
+    ("stress", torch.bfloat16, 1)])      # general path, 16,384 workgroups
 def test_fused_other_dtype_and_alignment(built, name, dtype, offset):
     wl, clf, orc = built(name)
     states = wl.states(9)
