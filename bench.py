@@ -473,8 +473,9 @@ def measured_traffic(workload: str, kernel: str):
     """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
     None when there is none for this workload or the kernel source changed
     since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"{workload}_c3_pmc_traffic.md" if workload == "schema" else
-                        f"{workload}_pmc_traffic.md")
+    tag = {"arithmetic": "arithmetic_c1", "json": "json_c2", "schema": "schema_c3", "pylike": "pylike_c4",
+           "stress": "stress_c5"}.get(workload, workload)
+    path = os.path.join(ROOT, "profiles", f"{tag}_pmc_traffic.md")
     if not os.path.exists(path):
         return None
     meta = None
