@@ -33,6 +33,87 @@ class PscError(RuntimeError):
         self.status = status
 
 
+# Argument checks (not asserts, so that python -O keeps them): the library
+# trusts the sizes it is given, so a tensor of the wrong shape, dtype or
+# device must never reach it.  (The lengths of ragged stacks live on the
+# device and are not checked here: `stacks` must hold their sum.)
+def _require(ok: bool, what: str) -> None:
+    if not ok:
+        raise ValueError(f"psc: expected {what}")
+
+
+_T = {}   # torch types, looked up once
+
+
+def _torch_types():
+    if not _T:
+        import torch
+        _T.update(tensor=torch.Tensor, i32=torch.int32,
+                  codes={torch.float32: PSC_F32, torch.bfloat16: PSC_BF16})
+    return _T
+
+
+def _i32(t, name: str, dev: int, numel: int | None = None, shape: tuple | None = None):
+    """t as a contiguous int32 tensor on device index `dev` (get_device(): -1
+    for host memory), with numel elements or the given shape."""
+    T = _T or _torch_types()
+    # one cheap test on the common path; the message is built only on failure
+    if (type(t) is T["tensor"] and t.dtype is T["i32"] and t.get_device() == dev and t.is_contiguous()
+            and (numel is None or t.numel() == numel) and (shape is None or t.shape == shape)):
+        return t
+    _require(isinstance(t, T["tensor"]) and t.dtype is T["i32"] and t.is_contiguous(),
+             f"{name} to be a contiguous int32 tensor")
+    _require(t.get_device() == dev, f"{name} on device {dev} (the bound device), not {t.get_device()}")
+    _require(numel is None or t.numel() == numel, f"{name} to hold {numel} elements, not {t.numel()}")
+    _require(shape is None or tuple(t.shape) == tuple(shape),
+             f"{name} of shape {shape and tuple(shape)}, not {tuple(t.shape)}")
+    return t
+
+
+def _logits(t, dev: int, B: int, V: int) -> int:
+    """The dtype code of contiguous logits [B, V] on device index `dev`."""
+    T = _T or _torch_types()
+    code = T["codes"].get(getattr(t, "dtype", None))
+    if (code is not None and type(t) is T["tensor"] and t.get_device() == dev and t.is_contiguous()
+            and t.shape == (B, V)):
+        return code
+    _require(isinstance(t, T["tensor"]) and t.is_contiguous() and tuple(t.shape) == (B, V),
+             f"logits to be a contiguous tensor of shape ({B}, {V})")
+    _require(t.get_device() == dev, f"logits on device {dev} (the bound device), not {t.get_device()}")
+    _require(code is not None, f"float32 or bfloat16 logits, not {t.dtype}")
+    return code
+
+
+def _step_args(dev: int, stacks, lens, qs, logits=None, V: int = 0, out=None, out_cols: int = 0):
+    """The checks of one mask-step call in one test on the common path:
+    ragged states, optional logits [B, V], optional int32 out ([B, out_cols],
+    or [B] when out_cols is 0).  Returns (B, logits dtype code or None)."""
+    T = _T or _torch_types()
+    i32 = T["i32"]
+    try:
+        B = lens.numel()
+        code = T["codes"].get(logits.dtype) if logits is not None else None
+        ok = (lens.dtype is i32 and lens.get_device() == dev and lens.is_contiguous()
+              and qs.dtype is i32 and qs.get_device() == dev and qs.is_contiguous() and qs.numel() == B
+              and stacks.dtype is i32 and stacks.get_device() == dev and stacks.is_contiguous()
+              and (logits is None or (code is not None and logits.get_device() == dev and logits.is_contiguous()
+                                      and logits.shape == (B, V)))
+              and (out is None or (out.dtype is i32 and out.get_device() == dev and out.is_contiguous()
+                                   and out.shape == ((B, out_cols) if out_cols else (B,)))))
+    except AttributeError:
+        ok = False
+    if ok:
+        return B, code
+    # the slow path names what is wrong
+    B = int(_i32(lens, "stack_lens", dev).numel())
+    _i32(qs, "lexer_states", dev, numel=B)
+    _i32(stacks, "stacks", dev)
+    code = _logits(logits, dev, B, V) if logits is not None else None
+    if out is not None:
+        _i32(out, "out", dev, shape=(B, out_cols) if out_cols else (B,))
+    return B, code
+
+
 class _Grammar(C.Structure):
     _fields_ = [
         ("n_lex_states", C.c_int32), ("lex_next", C.c_void_p), ("lex_accept", C.c_void_p),
@@ -222,19 +303,33 @@ class Classifier:
         buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
         off = (-buf.data_ptr()) % 256
         self._dev = buf
+        self._device = buf.device
+        self._dev_index = buf.get_device()
         self._dev_ptr = buf.data_ptr() + off
         _check(lib().psc_bind_device(self._h, self._dev_ptr, n, _stream_ptr(stream)))
         return self
 
+    @property
+    def device(self):
+        """The device the tables are bound to (PSC_E_NOT_BOUND before bind)."""
+        dev = getattr(self, "_device", None)
+        if dev is None:
+            raise PscError(-6, "the classifier is not bound to a device (call bind first)")
+        return dev
+
+    @property
+    def _idx(self) -> int:
+        idx = getattr(self, "_dev_index", None)
+        if idx is None:
+            raise PscError(-6, "the classifier is not bound to a device (call bind first)")
+        return idx
+
     def compute_masks(self, stacks, stack_lens, lexer_states, out=None, stream=None):
         """Device int32 tensors -> uint32 bitmask [B, W] (torch.int32 view)."""
         import torch
-        B = int(stack_lens.shape[0])
-        for t in (stacks, stack_lens, lexer_states):
-            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
         if out is None:
-            out = torch.empty((B, self.W), dtype=torch.int32, device=stack_lens.device)
-        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and tuple(out.shape) == (B, self.W)
+            out = torch.empty((int(stack_lens.shape[0]), self.W), dtype=torch.int32, device=self.device)
+        B, _ = _step_args(self._idx, stacks, stack_lens, lexer_states, out=out, out_cols=self.W)
         _check(lib().psc_compute_masks(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
                                        lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
@@ -242,12 +337,9 @@ class Classifier:
     def compute_classes(self, stacks, stack_lens, lexer_states, out=None, stream=None):
         """Device int32 tensors -> class ids int32 [B] (-1 for a rejected input)."""
         import torch
-        B = int(stack_lens.shape[0])
-        for t in (stacks, stack_lens, lexer_states):
-            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
         if out is None:
-            out = torch.empty(B, dtype=torch.int32, device=stack_lens.device)
-        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and out.numel() == B
+            out = torch.empty(int(stack_lens.shape[0]), dtype=torch.int32, device=self.device)
+        B, _ = _step_args(self._idx, stacks, stack_lens, lexer_states, out=out)
         _check(lib().psc_compute_classes(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
                                          lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
@@ -255,16 +347,8 @@ class Classifier:
     def compute_and_apply(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
         """One launch: masks for the B prefix states applied to logits [B, V] in
         place; the bitmask is also written to `out` when given.  Returns logits."""
-        import torch
-        B = int(stack_lens.shape[0])
-        for t in (stacks, stack_lens, lexer_states):
-            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
-        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (B, self.V)
-        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
-        out_ptr = None
-        if out is not None:
-            assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and tuple(out.shape) == (B, self.W)
-            out_ptr = out.data_ptr()
+        B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out, self.W)
+        out_ptr = None if out is None else out.data_ptr()
         _check(lib().psc_compute_and_apply(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
                                            lexer_states.data_ptr(), B, out_ptr, logits.data_ptr(), dt,
                                            self.V, _stream_ptr(stream)))
@@ -274,14 +358,9 @@ class Classifier:
         """Greedy token per sequence under its mask (int32 [B]; -1 = none
         allowed); the logits are only read."""
         import torch
-        B = int(stack_lens.shape[0])
-        for t in (stacks, stack_lens, lexer_states):
-            assert t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()
-        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (B, self.V)
-        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
         if out is None:
-            out = torch.empty(B, dtype=torch.int32, device=logits.device)
-        assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous() and out.numel() == B
+            out = torch.empty(int(stack_lens.shape[0]), dtype=torch.int32, device=self.device)
+        B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out)
         _check(lib().psc_compute_and_argmax(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
                                             lexer_states.data_ptr(), B, logits.data_ptr(), dt, self.V,
                                             out.data_ptr(), _stream_ptr(stream)))
@@ -304,6 +383,7 @@ class DecodeStates:
         self.lens = torch.zeros(self.B, dtype=torch.int32, device=device)
         self.qs = torch.zeros(self.B, dtype=torch.int32, device=device)
         self.status = torch.zeros(self.B, dtype=torch.int32, device=device)
+        _require(self.stacks.device == clf.device, f"the states on the classifier's device {clf.device}")
         self.reset(stream)
 
     def reset(self, stream=None):
@@ -315,10 +395,10 @@ class DecodeStates:
     def load(self, states):
         """Set the states from host (q, stack bottom->top) pairs."""
         import torch
-        assert len(states) == self.B
+        _require(len(states) == self.B, f"{self.B} states, not {len(states)}")
         st = np.zeros((self.B, self.cap), np.int32)
         for b, (q, a) in enumerate(states):
-            assert 1 <= len(a) <= self.cap
+            _require(1 <= len(a) <= self.cap, f"stacks of 1 to {self.cap} symbols, not {len(a)}")
             st[b, :len(a)] = a
         self.stacks.copy_(torch.from_numpy(st))
         self.lens.copy_(torch.tensor([len(a) for _, a in states], dtype=torch.int32))
@@ -328,8 +408,7 @@ class DecodeStates:
     def advance(self, tokens, stream=None):
         """One token per sequence (int32 device tensor [B], < 0 = skip);
         returns the status tensor (ADV_*)."""
-        import torch
-        assert tokens.is_cuda and tokens.dtype == torch.int32 and tokens.numel() == self.B
+        _i32(tokens, "tokens", self.clf._idx, numel=self.B)
         _check(lib().psc_advance(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
                                  self.qs.data_ptr(), self.B, tokens.data_ptr(), self.status.data_ptr(),
                                  _stream_ptr(stream)))
@@ -339,7 +418,7 @@ class DecodeStates:
         import torch
         if out is None:
             out = torch.empty((self.B, self.clf.W), dtype=torch.int32, device=self.lens.device)
-        assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
+        _i32(out, "out", self.clf._idx, shape=(self.B, self.clf.W))
         _check(lib().psc_compute_masks_dense(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
                                              self.qs.data_ptr(), self.B, out.data_ptr(), _stream_ptr(stream)))
         return out
@@ -348,19 +427,16 @@ class DecodeStates:
         import torch
         if out is None:
             out = torch.empty(self.B, dtype=torch.int32, device=self.lens.device)
-        assert out.is_contiguous() and out.numel() == self.B and out.dtype == torch.int32
+        _i32(out, "out", self.clf._idx, numel=self.B)
         _check(lib().psc_compute_classes_dense(self.clf._h, self.stacks.data_ptr(), self.cap, self.lens.data_ptr(),
                                                self.qs.data_ptr(), self.B, out.data_ptr(), _stream_ptr(stream)))
         return out
 
     def compute_and_apply(self, logits, out=None, stream=None):
-        import torch
-        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
-        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        dt = _logits(logits, self.clf._idx, self.B, self.clf.V)
         out_ptr = None
         if out is not None:
-            assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
-            out_ptr = out.data_ptr()
+            out_ptr = _i32(out, "out", self.clf._idx, shape=(self.B, self.clf.W)).data_ptr()
         _check(lib().psc_compute_and_apply_dense(self.clf._h, self.stacks.data_ptr(), self.cap,
                                                  self.lens.data_ptr(), self.qs.data_ptr(), self.B, out_ptr,
                                                  logits.data_ptr(), dt, self.clf.V, _stream_ptr(stream)))
@@ -369,10 +445,10 @@ class DecodeStates:
     def argmax(self, logits, out=None, stream=None):
         """Greedy token per sequence under its mask (int32 [B]; -1 = none)."""
         import torch
-        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
-        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        dt = _logits(logits, self.clf._idx, self.B, self.clf.V)
         if out is None:
             out = torch.empty(self.B, dtype=torch.int32, device=logits.device)
+        _i32(out, "out", self.clf._idx, numel=self.B)
         _check(lib().psc_compute_and_argmax_dense(self.clf._h, self.stacks.data_ptr(), self.cap,
                                                   self.lens.data_ptr(), self.qs.data_ptr(), self.B,
                                                   logits.data_ptr(), dt, self.clf.V, out.data_ptr(),
@@ -385,16 +461,23 @@ class DecodeStates:
         new states go to a second set of buffers, which then become this
         object's; returns the status tensor (ADV_*)."""
         import torch
-        assert tokens.is_cuda and tokens.dtype == torch.int32 and tokens.numel() == self.B
-        assert logits.is_cuda and logits.is_contiguous() and tuple(logits.shape) == (self.B, self.clf.V)
-        dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+        dev, T = self.clf._idx, (_T or _torch_types())
+        dt = T["codes"].get(getattr(logits, "dtype", None))
+        try:
+            ok = (tokens.dtype is T["i32"] and tokens.get_device() == dev and tokens.is_contiguous()
+                  and tokens.numel() == self.B and dt is not None and logits.get_device() == dev
+                  and logits.is_contiguous() and logits.shape == (self.B, self.clf.V))
+        except AttributeError:
+            ok = False
+        if not ok:      # names what is wrong
+            _i32(tokens, "tokens", dev, numel=self.B)
+            dt = _logits(logits, dev, self.B, self.clf.V)
         if getattr(self, "_spare", None) is None:
             self._spare = (torch.empty_like(self.stacks), torch.empty_like(self.lens), torch.empty_like(self.qs))
         so, lo, qo = self._spare
         out_ptr = None
         if out is not None:
-            assert out.is_contiguous() and tuple(out.shape) == (self.B, self.clf.W) and out.dtype == torch.int32
-            out_ptr = out.data_ptr()
+            out_ptr = _i32(out, "out", self.clf._idx, shape=(self.B, self.clf.W)).data_ptr()
         _check(lib().psc_decode_step(self.clf._h, self.stacks.data_ptr(), self.lens.data_ptr(), self.qs.data_ptr(),
                                      so.data_ptr(), lo.data_ptr(), qo.data_ptr(), self.cap, self.B,
                                      tokens.data_ptr(), self.status.data_ptr(), out_ptr, logits.data_ptr(), dt,
@@ -414,9 +497,10 @@ class DecodeStates:
 def apply_mask(logits, bitmask, stream=None):
     """In place: logits[b, v] = -inf where bit v of bitmask[b] is 0."""
     import torch
-    assert logits.is_cuda and logits.is_contiguous() and logits.dim() == 2
+    _require(isinstance(logits, torch.Tensor) and logits.is_cuda and logits.dim() == 2,
+             "logits to be a 2-D device tensor")
     B, V = logits.shape
-    assert bitmask.is_cuda and bitmask.is_contiguous() and tuple(bitmask.shape) == (B, (V + 31) // 32)
-    dt = {torch.float32: PSC_F32, torch.bfloat16: PSC_BF16}[logits.dtype]
+    dt = _logits(logits, logits.get_device(), B, V)
+    _i32(bitmask, "bitmask", logits.get_device(), shape=(B, (V + 31) // 32))
     _check(lib().psc_apply_mask(logits.data_ptr(), dt, bitmask.data_ptr(), B, V, _stream_ptr(stream)))
     return logits

@@ -143,3 +143,36 @@ def test_build_is_deterministic():
         rows = np.stack([clf.class_mask(c) for c in range(inf["n_classes"])])
         outs.append((clf.classify_host(states).tobytes(), rows.tobytes(), inf["table_bytes"]))
     assert outs[0] == outs[1] == outs[2]
+
+
+def test_binding_rejects_bad_tensors_before_the_library():
+    """The binding's argument checks are explicit (they hold under python -O)
+    and fire before any call into the library: wrong dtype, shape, layout or
+    device (device indices as torch's get_device(): -1 is host memory)."""
+    import torch
+    from paper_2608_03065_amd import psc
+    ok = torch.zeros(4, dtype=torch.int32)
+    assert psc._i32(ok, "x", -1, numel=4) is ok
+    with pytest.raises(ValueError):
+        psc._i32(torch.zeros(4, dtype=torch.int64), "x", -1)
+    with pytest.raises(ValueError):
+        psc._i32(ok, "x", -1, numel=5)
+    with pytest.raises(ValueError):
+        psc._i32(torch.zeros((2, 3), dtype=torch.int32), "x", -1, shape=(3, 2))
+    with pytest.raises(ValueError):
+        psc._i32(torch.zeros((2, 3), dtype=torch.int32).t(), "x", -1)
+    with pytest.raises(ValueError):
+        psc._i32(ok, "x", 0)                      # host memory where device 0 is bound
+    with pytest.raises(ValueError):
+        psc._i32([0, 1], "x", -1)
+    with pytest.raises(ValueError):
+        psc._logits(torch.zeros((2, 5), dtype=torch.float16), -1, 2, 5)
+    with pytest.raises(ValueError):
+        psc._logits(torch.zeros((2, 4), dtype=torch.float32), -1, 2, 5)
+    assert psc._logits(torch.zeros((2, 5), dtype=torch.bfloat16), -1, 2, 5) == psc.PSC_BF16
+    # an unbound classifier reports PSC_E_NOT_BOUND, as the library would
+    wl = configs.get("arithmetic")
+    clf = Classifier(wl.grammar, wl.vocab)
+    with pytest.raises(PscError) as e:
+        clf.compute_masks(ok, ok, ok)
+    assert e.value.status == -6
