@@ -916,7 +916,7 @@ using namespace psc;
 
 size_t psc_handle::device_bytes_needed() const {
     auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
-    return kTableOff + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
+    return psc::table_off(n_lex) + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
            up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes +
            up((size_t)n_lr * adv.n_term * sizeof(int32_t)) + up(psc::goto_closure_bytes(*this));
 }
@@ -970,6 +970,26 @@ void goto_closure(const psc_handle &h, std::vector<int32_t> &out) {
                 row[t] = x;
             }
         }
+}
+
+void start_blocks(const psc_handle &h, std::vector<int32_t> &out) {
+    out.assign((size_t)h.n_lex * kStartBlockInts, 0);
+    const int64_t T = (int64_t)h.table.size();
+    auto at = [&](int64_t i) { return i < T ? h.table[(size_t)i] : 0; };
+    for (int32_t q = 0; q < h.n_lex; q++) {
+        const int32_t ref = h.table[(size_t)q];
+        if (ref < 0 || (ref & 3) == kRefDense) continue;
+        const int64_t row = ref & ~3;
+        int32_t *blk = out.data() + (size_t)q * kStartBlockInts;
+        for (int lane = 0; lane < 64; lane++) {
+            if ((ref & 3) == kRefChain) {
+                for (int k = 0; k < kChainEntry; k++) blk[4 * lane + k] = at(row + kChainEntry * lane + k);
+            } else {
+                blk[4 * lane] = at(row + 2 * lane);
+                blk[4 * lane + 1] = at(row + 2 * lane + 1);
+            }
+        }
+    }
 }
 }  // namespace psc
 

@@ -172,6 +172,15 @@ struct Walk {
         return false;
     }
 
+    // The first step from start[q], whose wavefront load (the start block)
+    // was fetched together with the window; a dense row still reads its entry.
+    __device__ __forceinline__ bool first_step(const int4 blk) {
+        if ((ref & 3) == kRefChain) return chain_step(blk);
+        if ((ref & 3) == kRefDense) return step();
+        const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
+        return row_step(make_int2(blk.x, blk.y), X);
+    }
+
     // One step: the one table load, then its evaluation.  A chain or sparse
     // row is loaded before the window is read.
     __device__ __forceinline__ bool step() {
@@ -193,16 +202,23 @@ struct Walk {
     }
 };
 
+// The start blocks sit just below the table: block q (kStartBlockInts int32)
+// starts (n_lex - q) blocks before it.
 template <bool kOverlay = false>
-__device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lr,
+__device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                           const int32_t *__restrict__ st, int len, int q, int lane,
                                           const int32_t *ov = nullptr, int ptr = 0) {
     Walk<kOverlay> w{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1, ov, ptr};
-    // round trip 2: the window, with start[q] in lane 63
+    // round trip 2: the window, with start[q] in lane 63, and start[q]'s
+    // first wavefront load from the start block
+    int4 blk = reinterpret_cast<const int4 *>(table - (int64_t)(n_lex - q) * kStartBlockInts)[lane];
     w.sym = lane == kChunk ? table[q] : w.load(max(w.chunk_base - lane, 0));
+    // both loads are needed here: this keeps the compiler from sinking the
+    // block's load below the wait for the window
+    asm volatile("" : "+v"(blk.x), "+v"(blk.y), "+v"(blk.z), "+v"(blk.w), "+v"(w.sym));
     w.ref = __builtin_amdgcn_readlane(w.sym, kChunk);
     if (w.ref < 0) return -w.ref - 1;
-    if (w.step()) return w.cls;
+    if (w.first_step(blk)) return w.cls;
     for (;;) {
         // ref, i and chunk_base are wave-uniform; saying so keeps the
         // loop's branches scalar
@@ -262,7 +278,7 @@ __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int
     const int q = __builtin_amdgcn_readlane(own, 1);
     const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
     if (len > 0 && (stride == 0 || len <= stride) && q >= 0 && q < n_lex)
-        return walk_class(table, n_lr, stacks + off, len, q, lane);
+        return walk_class(table, n_lex, n_lr, stacks + off, len, q, lane);
     return -1;
 }
 
@@ -874,7 +890,7 @@ __device__ __forceinline__ int decode_block_class(const int32_t *__restrict__ ta
         }
         int cls = -1;
         if (new_len > 0 && new_len <= cap && q >= 0 && q < D.T.n_lex)
-            cls = walk_class<true>(table, D.T.n_lr, st, new_len, q, lane, s_ov, ptr);
+            cls = walk_class<true>(table, D.T.n_lex, D.T.n_lr, st, new_len, q, lane, s_ov, ptr);
         if (lane == 0) {
             s_cls = cls;
             if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
@@ -964,7 +980,7 @@ psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t st
     const int vec4 = (W % 4 == 0) && ((reinterpret_cast<uintptr_t>(out_bitmask) & 15) == 0);
     dim3 grid((W + kCopyWordsPerBlock - 1) / kCopyWordsPerBlock, B);
     hipLaunchKernelGGL(walk_gather_kernel, grid, dim3(kBlock), 0, reinterpret_cast<hipStream_t>(stream),
-                       reinterpret_cast<const int32_t *>(base + kTableOff),
+                       reinterpret_cast<const int32_t *>(base + table_off(h->n_lex)),
                        reinterpret_cast<const uint32_t *>(base + h->mask_off), h->mask_stride, h->n_lex, h->n_lr,
                        stacks, stride, stack_lens, lexer_states, B, W, out_bitmask,
                        reinterpret_cast<uint32_t *>(base), vec4);
@@ -985,7 +1001,7 @@ psc_status launch_classes(const psc_handle *h, const int32_t *stacks, int32_t st
     char *base = static_cast<char *>(h->dev_base);
     const int per_block = kBlock / kWave;
     hipLaunchKernelGGL(classes_kernel, dim3((B + per_block - 1) / per_block), dim3(kBlock), 0,
-                       reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const int32_t *>(base + kTableOff),
+                       reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const int32_t *>(base + table_off(h->n_lex)),
                        h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, B, out_classes,
                        reinterpret_cast<uint32_t *>(base));
     hipError_t e = hipGetLastError();
@@ -1014,7 +1030,7 @@ psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stri
     if (B == 0) return PSC_OK;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
     const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
     uint32_t *err = reinterpret_cast<uint32_t *>(base);
     const int32_t W = h->W;
@@ -1068,7 +1084,7 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
     if (B == 0) return PSC_OK;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
     const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
     uint32_t *err = reinterpret_cast<uint32_t *>(base);
     const int fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
@@ -1146,7 +1162,8 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(dev_buf);
-    const size_t mask_off = kTableOff + up(h->table.size() * sizeof(int32_t));
+    const size_t tab_off = table_off(h->n_lex);
+    const size_t mask_off = tab_off + up(h->table.size() * sizeof(int32_t));
     const size_t gram_off = mask_off + up(h->masks.size() * sizeof(uint32_t));
     const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
     const size_t argmax_off = vbytes_off + up(h->vbytes.size());
@@ -1156,10 +1173,15 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     const size_t closure_off = packed_off + up((size_t)h->n_lr * h->adv.n_term * sizeof(int32_t));
     std::vector<int32_t> closure;
     goto_closure(*h, closure);
-    hipError_t e = hipMemsetAsync(base, 0, kTableOff, s);
+    std::vector<int32_t> blocks;
+    start_blocks(*h, blocks);
+    hipError_t e = hipMemsetAsync(base, 0, kStartBlockOff, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(base + kStartBlockOff, blocks.data(), blocks.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemsetAsync(base + argmax_off, 0, kArgmaxBytes, s);
     if (e == hipSuccess)
-        e = hipMemcpyAsync(base + kTableOff, h->table.data(), h->table.size() * sizeof(int32_t),
+        e = hipMemcpyAsync(base + tab_off, h->table.data(), h->table.size() * sizeof(int32_t),
                            hipMemcpyHostToDevice, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + mask_off, h->masks.data(), h->masks.size() * sizeof(uint32_t),
@@ -1315,7 +1337,7 @@ extern "C" psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks
     }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + kTableOff);
+    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
     const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
     uint32_t *err = reinterpret_cast<uint32_t *>(base);
     const DecodeArgs D{adv_tables(h), stacks_in, lens_in, qs_in, stacks_out, lens_out, qs_out, tokens, status, cap};

@@ -71,7 +71,11 @@ struct AdvanceLayout {
 
 // Device buffer layout (offsets in bytes from the bound base):
 //   [0, 256)                   uint32 error counter (+ padding)
-//   [kTableOff, ...)           int32 table: start refs [n_lex], rows, pad
+//   [256, table_off(n_lex))    start blocks [n_lex][64 lanes][4] int32: block q holds the
+//                              first walk step's wavefront load from start[q] (the 64
+//                              chain entries, or the sparse row's pairs in .x/.y), so that
+//                              it is fetched together with the stack instead of after it
+//   [table_off(n_lex), ...)    int32 table: start refs [n_lex], rows, pad
 //   [mask_off, ...)            uint32 masks [n_classes][mask_stride] (256-B aligned)
 //   [gram_off, ...)            int32 advance blob (AdvanceLayout)
 //   [vbytes_off, ...)          uint8 vocabulary bytes
@@ -79,7 +83,11 @@ struct AdvanceLayout {
 //                              slot then a uint32 arrival counter (zero between calls)
 //   [packed_off, ...)          int32 ACTION with packed reductions (packed_action)
 //   [closure_off, ...)         int32 unit-reduction closure of GOTO (goto_closure), when it fits
-constexpr size_t kTableOff = 256;
+constexpr size_t kStartBlockOff = 256;
+constexpr int kStartBlockInts = 64 * 4;   // one 16-byte vector per lane
+constexpr size_t table_off(int32_t n_lex) {
+    return kStartBlockOff + (size_t)n_lex * kStartBlockInts * sizeof(int32_t);
+}
 constexpr size_t kArgmaxSlots = 65536;
 constexpr size_t kArgmaxRecordWords = 16;   // uint64 words per record: one 128-byte cache line
 constexpr size_t kArgmaxBytes = kArgmaxSlots * kArgmaxRecordWords * sizeof(unsigned long long);
@@ -122,6 +130,11 @@ bool packed_action(const psc_handle &h, std::vector<int32_t> &out);
 constexpr size_t kClosureMaxBytes = 64u << 20;
 size_t goto_closure_bytes(const psc_handle &h);
 void goto_closure(const psc_handle &h, std::vector<int32_t> &out);
+// The start blocks, [n_lex][kStartBlockInts]: block q is what a walk's
+// first step from start[q] loads, one 16-byte vector per lane (a chain
+// entry's 64 entries as they are; a sparse row's int32 pairs in .x/.y);
+// zeros for a determined start or a dense row, which the walk does not read.
+void start_blocks(const psc_handle &h, std::vector<int32_t> &out);
 // The input checks of psc_build (ids in range, spellings), for loaded tables.
 psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg);
 }
