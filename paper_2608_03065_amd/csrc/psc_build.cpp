@@ -973,10 +973,11 @@ void goto_closure(const psc_handle &h, std::vector<int32_t> &out) {
 }
 
 void start_blocks(const psc_handle &h, std::vector<int32_t> &out) {
-    out.assign((size_t)h.n_lex * kStartBlockInts, 0);
+    const int32_t nb = start_block_count(h.n_lex);
+    out.assign((size_t)nb * kStartBlockInts, 0);
     const int64_t T = (int64_t)h.table.size();
     auto at = [&](int64_t i) { return i < T ? h.table[(size_t)i] : 0; };
-    for (int32_t q = 0; q < h.n_lex; q++) {
+    for (int32_t q = 0; q < nb; q++) {
         const int32_t ref = h.table[(size_t)q];
         if (ref < 0 || (ref & 3) == kRefDense) continue;
         const int64_t row = ref & ~3;

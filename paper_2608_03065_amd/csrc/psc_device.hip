@@ -50,6 +50,7 @@ __device__ __forceinline__ int64_t wave_sum(int64_t v) {
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Streaming (non-temporal) 16-byte accesses: the logits and mask rows are
 // touched once per step, so they should not evict the classifier table.
@@ -203,7 +204,9 @@ struct Walk {
 };
 
 // The start blocks sit just below the table: block q (kStartBlockInts int32)
-// starts (n_lex - q) blocks before it.
+// starts (nb - q) blocks before it, nb = start_block_count(n_lex) (n_lex >= 1
+// here: q is in range).  A higher q loads block nb - 1 in its place and
+// takes its first step as any other.
 template <bool kOverlay = false>
 __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
                                           const int32_t *__restrict__ st, int len, int q, int lane,
@@ -211,14 +214,22 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
     Walk<kOverlay> w{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1, ov, ptr};
     // round trip 2: the window, with start[q] in lane 63, and start[q]'s
     // first wavefront load from the start block
-    int4 blk = reinterpret_cast<const int4 *>(table - (int64_t)(n_lex - q) * kStartBlockInts)[lane];
+    const int nb = start_block_count(n_lex);
+    u32x4 bv = reinterpret_cast<const u32x4 *>(table - (int64_t)(nb - min(q, nb - 1)) * kStartBlockInts)[lane];
     w.sym = lane == kChunk ? table[q] : w.load(max(w.chunk_base - lane, 0));
-    // both loads are needed here: this keeps the compiler from sinking the
-    // block's load below the wait for the window
-    asm volatile("" : "+v"(blk.x), "+v"(blk.y), "+v"(blk.z), "+v"(blk.w), "+v"(w.sym));
+    // both loads are needed here, as whole registers: this keeps the compiler
+    // from sinking the block's load below the wait for the window, or waiting
+    // for it before the window's load is issued
+    asm volatile("" : "+v"(bv), "+v"(w.sym));
     w.ref = __builtin_amdgcn_readlane(w.sym, kChunk);
     if (w.ref < 0) return -w.ref - 1;
-    if (w.first_step(blk)) return w.cls;
+    if (q >= nb) {
+        // no start block: the same load from the row itself
+        const int32_t *row = table + (w.ref & ~3);
+        if ((w.ref & 3) == kRefChain) bv = *reinterpret_cast<const u32x4 *>(row + kChainEntry * lane);
+        else if ((w.ref & 3) != kRefDense) bv.xy = *reinterpret_cast<const u32x2 *>(row + 2 * lane);
+    }
+    if (w.first_step(make_int4((int)bv[0], (int)bv[1], (int)bv[2], (int)bv[3]))) return w.cls;
     for (;;) {
         // ref, i and chunk_base are wave-uniform; saying so keeps the
         // loop's branches scalar

@@ -71,7 +71,7 @@ struct AdvanceLayout {
 
 // Device buffer layout (offsets in bytes from the bound base):
 //   [0, 256)                   uint32 error counter (+ padding)
-//   [256, table_off(n_lex))    start blocks [n_lex][64 lanes][4] int32: block q holds the
+//   [256, table_off(n_lex))    start blocks [min(n_lex, kMaxStartBlocks)][64 lanes][4] int32: block q holds the
 //                              first walk step's wavefront load from start[q] (the 64
 //                              chain entries, or the sparse row's pairs in .x/.y), so that
 //                              it is fetched together with the stack instead of after it
@@ -85,8 +85,12 @@ struct AdvanceLayout {
 //   [closure_off, ...)         int32 unit-reduction closure of GOTO (goto_closure), when it fits
 constexpr size_t kStartBlockOff = 256;
 constexpr int kStartBlockInts = 64 * 4;   // one 16-byte vector per lane
+// Lexer states q < kMaxStartBlocks have a start block (at most 4 MB); a walk
+// from a higher one reads start[q]'s row after start[q], as any other row.
+constexpr int32_t kMaxStartBlocks = 4096;
+constexpr int32_t start_block_count(int32_t n_lex) { return n_lex < kMaxStartBlocks ? n_lex : kMaxStartBlocks; }
 constexpr size_t table_off(int32_t n_lex) {
-    return kStartBlockOff + (size_t)n_lex * kStartBlockInts * sizeof(int32_t);
+    return kStartBlockOff + (size_t)start_block_count(n_lex) * kStartBlockInts * sizeof(int32_t);
 }
 constexpr size_t kArgmaxSlots = 65536;
 constexpr size_t kArgmaxRecordWords = 16;   // uint64 words per record: one 128-byte cache line
@@ -130,7 +134,7 @@ bool packed_action(const psc_handle &h, std::vector<int32_t> &out);
 constexpr size_t kClosureMaxBytes = 64u << 20;
 size_t goto_closure_bytes(const psc_handle &h);
 void goto_closure(const psc_handle &h, std::vector<int32_t> &out);
-// The start blocks, [n_lex][kStartBlockInts]: block q is what a walk's
+// The start blocks, [start_block_count(n_lex)][kStartBlockInts]: block q is what a walk's
 // first step from start[q] loads, one 16-byte vector per lane (a chain
 // entry's 64 entries as they are; a sparse row's int32 pairs in .x/.y);
 // zeros for a determined start or a dense row, which the walk does not read.

@@ -282,3 +282,87 @@ def test_deep_right_recursive_stacks():
             assert got[b][0] == st[0] and np.array_equal(got[b][1], st[1]), b
     assert len(got[2][1]) == 4            # the whole chain of a's reduced
     assert clf.error_count() == 0
+
+
+# ------------------------------------------------- many lexer states
+
+@functools.lru_cache(maxsize=None)
+def _keywords():
+    """s -> item | s "," item, item -> one of 600 literal 12-letter keywords:
+    a lexer of 6,403 states (a trie of the keywords), more than the first
+    4,096 that get a start block on the device, so walks start from lexer
+    states on both sides of that limit.  The vocabulary has the letters,
+    ',' and ' ', pieces of keywords (which end deep in the trie) and EOS."""
+    rng = np.random.default_rng(7)
+    kws = set()
+    while len(kws) < 600:
+        kws.add("".join(rng.choice(list("abcdefghijklmnopqrstuvwxyz"), size=12)))
+    kws = sorted(kws)
+    g = Grammar("s")
+    g.ignore("WS", " +")
+    g.rule("s", "item", 's "," item')
+    g.rule("item", *['"%s"' % k for k in kws])
+    G = g.compile()
+    toks = [bytes([c]) for c in b"abcdefghijklmnopqrstuvwxyz, "]
+    pieces = {k[i:i + n].encode() for k in kws[:200]
+              for i, n in [(int(rng.integers(0, 8)), int(rng.integers(2, 6)))]}
+    toks += sorted(pieces - set(toks)) + [b""]
+    voc = Vocab(tokens=toks, eos_id=len(toks) - 1)
+    hp = HostParser(G)
+    docs = [",".join(kws[int(x)] for x in rng.integers(0, len(kws), size=3)).encode() for _ in range(256)]
+    states = [hp.state(d[:int(rng.integers(1, len(d) + 1))]) for d in docs]
+    return G, voc, docs, states, Oracle(G, voc)
+
+
+def test_many_lexer_states_host_walk():
+    G, voc, _, states, orc = _keywords()
+    from paper_2608_03065_amd.psc import Classifier
+    clf = Classifier(G, voc)
+    assert clf.info()["n_lex_states"] > 4096
+    qs = np.array([q for q, _ in states])
+    assert (qs >= 4096).sum() > 50 and (qs < 4096).sum() > 50
+    assert np.array_equal(clf.masks_host(states), orc.masks(states))
+
+
+@pytest.mark.gpu
+def test_many_lexer_states_on_device():
+    """The walk from lexer states with and without a start block: masks
+    (two-launch and fused paths, ragged stacks), the masked logits, and
+    the decoding step (advance, then a walk that reads the pushed states
+    from LDS) along the documents, all against the oracle."""
+    import torch
+    from paper_2608_03065_amd.psc import Classifier, DecodeStates, pack_states
+    G, voc, docs, states, orc = _keywords()
+    clf = Classifier(G, voc)
+    clf.bind(DEV)
+    V, B = len(voc.tokens), len(states)
+    want = orc.masks(states)
+    stacks, lens, qs = pack_states(states, DEV)
+    assert np.array_equal(clf.compute_masks(stacks, lens, qs).cpu().numpy().view(np.uint32), want)
+    x = torch.randn(B, V, generator=torch.Generator().manual_seed(9))
+    lg = x.to(DEV)
+    bm = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
+    clf.compute_and_apply(stacks, lens, qs, lg, out=bm)
+    assert np.array_equal(bm.cpu().numpy().view(np.uint32), want)
+    bits = np.unpackbits(want.astype("<u4").view(np.uint8), axis=1, bitorder="little")[:, :V].astype(bool)
+    ref = np.where(bits, x.numpy(), -np.inf).astype(np.float32)
+    assert np.array_equal(lg.cpu().numpy().view(np.int32), ref.view(np.int32))
+    # decoding along the documents, one token per step
+    ids = [voc.tokenize(d) for d in docs]
+    cap = 16
+    ds = DecodeStates(clf, B, cap, DEV).load([(0, np.array([0], np.int32))] * B)
+    host = [(0, np.array([0], np.int32))] * B
+    out = torch.empty((B, clf.W), dtype=torch.int32, device=DEV)
+    for k in range(max(len(t) for t in ids)):
+        tok = np.array([t[k] if k < len(t) else -1 for t in ids], np.int32)
+        lg = torch.zeros((B, V), dtype=torch.float32, device=DEV)
+        ds.decode_step(torch.from_numpy(tok).to(DEV), lg, out=out)
+        for b in range(B):
+            if tok[b] >= 0:
+                code, new = orc.advance(host[b], int(tok[b]))
+                assert code == Oracle.ADVANCED, (b, k)
+                host[b] = new
+        got = ds.host_states()
+        assert all(g[0] == h[0] and np.array_equal(g[1], h[1]) for g, h in zip(got, host)), k
+        assert np.array_equal(out.cpu().numpy().view(np.uint32), orc.masks(host)), k
+    assert clf.error_count() == 0
