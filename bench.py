@@ -49,7 +49,7 @@ def main():
                     help="also run a plain device copy of this many MiB (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1 "
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
                                    "(the mask path shards by batch or vocabulary with no exchange)"}))
         sys.exit(2)
 
