@@ -36,7 +36,7 @@ typedef enum {
     PSC_OK = 0,
     PSC_E_INVALID_ARG = -1, /* null pointer, negative size, inconsistent shape */
     PSC_E_GRAMMAR = -2,     /* malformed tables (ids out of range, empty spelling, ...) */
-    PSC_E_OOM = -4,         /* host allocation failed                                 */
+    PSC_E_OOM = -4,         /* host allocation failed (memory or threads)             */
     PSC_E_DEVICE = -5,      /* a HIP call or kernel launch failed                     */
     PSC_E_NOT_BOUND = -6,   /* device tables not bound (psc_bind_device)              */
     PSC_E_LIMIT = -7,       /* the construction exceeded a size limit                 */
@@ -158,7 +158,8 @@ size_t psc_device_bytes(const psc_handle *h);
  * nbytes >= psc_device_bytes, 256-byte aligned) on `stream`, and zero the
  * device error counter.  The buffer must stay alive and unmodified
  * while the handle is used; the handle keeps only the pointer.  Rebinding
- * replaces the previous binding.  Errors: PSC_E_INVALID_ARG, PSC_E_DEVICE.
+ * replaces the previous binding.  Errors: PSC_E_INVALID_ARG, PSC_E_DEVICE,
+ * PSC_E_OOM (the tables derived at bind time do not fit in host memory).
  */
 psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream);
 

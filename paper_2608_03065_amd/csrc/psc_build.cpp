@@ -43,6 +43,7 @@
 #include <cstring>
 #include <new>
 #include <stdexcept>
+#include <system_error>
 #include <unordered_map>
 
 #include "psc_internal.hpp"
@@ -1063,7 +1064,12 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             }
         };
         std::vector<std::thread> pool;
-        for (int32_t t = 1; t < n_threads; t++) pool.emplace_back(work, t);
+        try {
+            for (int32_t t = 1; t < n_threads; t++) pool.emplace_back(work, t);
+        } catch (const std::system_error &) {
+            // fewer threads than asked for: the lexer states are taken from a
+            // shared counter, so the threads that did start build all of them
+        }
         work(0);
         for (auto &th : pool) th.join();
         for (auto &e : errs)
@@ -1332,6 +1338,11 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         return e.code;
     } catch (const std::bad_alloc &) {
         set_error("psc_build: out of host memory");
+        return PSC_E_OOM;
+    } catch (const std::exception &e) {
+        // nothing may unwind through the C ABI; what is left is running out
+        // of host resources (a table too long for a vector, no thread)
+        set_error(std::string("psc_build: out of host resources (") + e.what() + ")");
         return PSC_E_OOM;
     }
 }

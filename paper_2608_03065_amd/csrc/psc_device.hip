@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <new>
 #include <string>
 
 #include "psc_internal.hpp"
@@ -1179,13 +1180,18 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
     const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
     const size_t argmax_off = vbytes_off + up(h->vbytes.size());
     const size_t packed_off = argmax_off + kArgmaxBytes;
-    std::vector<int32_t> packed;
-    const bool is_packed = packed_action(*h, packed);
     const size_t closure_off = packed_off + up((size_t)h->n_lr * h->adv.n_term * sizeof(int32_t));
-    std::vector<int32_t> closure;
-    goto_closure(*h, closure);
-    std::vector<int32_t> blocks;
-    start_blocks(*h, blocks);
+    // the tables derived at bind time, on the host first
+    std::vector<int32_t> packed, closure, blocks;
+    bool is_packed = false;
+    try {
+        is_packed = packed_action(*h, packed);
+        goto_closure(*h, closure);
+        start_blocks(*h, blocks);
+    } catch (const std::bad_alloc &) {
+        set_error("psc_bind_device: out of host memory");
+        return PSC_E_OOM;
+    }
     hipError_t e = hipMemsetAsync(base, 0, kStartBlockOff, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(base + kStartBlockOff, blocks.data(), blocks.size() * sizeof(int32_t),

@@ -18,7 +18,9 @@
 
 #include <cstdio>
 #include <cstring>
+#include <exception>
 #include <memory>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -280,6 +282,9 @@ extern "C" psc_status psc_save(const psc_handle *h, const char *path) {
     } catch (const std::bad_alloc &) {
         set_error("psc_save: out of host memory");
         return PSC_E_OOM;
+    } catch (const std::exception &e) {
+        set_error(std::string("psc_save: out of host resources (") + e.what() + ")");
+        return PSC_E_OOM;
     }
 }
 
@@ -332,6 +337,9 @@ extern "C" psc_status psc_load(const char *path, psc_handle **out) {
         return e.code;
     } catch (const std::bad_alloc &) {
         set_error("psc_load: out of host memory");
+        return PSC_E_OOM;
+    } catch (const std::exception &e) {
+        set_error(std::string("psc_load: out of host resources (") + e.what() + ")");
         return PSC_E_OOM;
     }
 }

@@ -176,3 +176,39 @@ def test_binding_rejects_bad_tensors_before_the_library():
     with pytest.raises(PscError) as e:
         clf.compute_masks(ok, ok, ok)
     assert e.value.status == -6
+
+
+_OOM_SCRIPT = r"""
+import resource, sys
+sys.path.insert(0, sys.argv[1])
+from inputs import configs
+from paper_2608_03065_amd import psc
+psc.lib()
+wl = configs.get("schema")
+G, voc = wl.grammar, wl.vocab
+vm = int([l for l in open("/proc/self/status") if l.startswith("VmSize")][0].split()[1]) * 1024
+soft, hard = resource.getrlimit(resource.RLIMIT_AS)
+resource.setrlimit(resource.RLIMIT_AS, (vm + (64 << 20), hard))
+try:
+    psc.Classifier(G, voc)
+    print("BUILT", flush=True)
+except psc.PscError as e:
+    print("STATUS", e.status, flush=True)
+resource.setrlimit(resource.RLIMIT_AS, (soft, hard))
+a = configs.get("arithmetic")
+print("AFTER", psc.Classifier(a.grammar, a.vocab).info()["n_lr_states"], flush=True)
+"""
+
+
+def test_build_reports_out_of_memory():
+    """An allocation failure inside psc_build (forced with an address-space
+    limit of 64 MB above what the process holds, far below what the schema
+    construction needs) is PSC_E_OOM, not a crash; the process then builds
+    another classifier normally."""
+    import subprocess
+    import sys
+    env = dict(os.environ, PSC_BUILD_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", _OOM_SCRIPT, ROOT], capture_output=True, text=True, timeout=300,
+                       env=env, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "STATUS -4" in r.stdout and "AFTER 12" in r.stdout, r.stdout
