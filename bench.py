@@ -147,6 +147,18 @@ def main():
         ms_per_step = loop(step, args.steps, warm=0) * 1e-3
         # (2) the other formulation of the same step, for comparison
         t_other = loop(other, min(args.steps, 1000))
+        # (2b) the spread: the same back-to-back loop cut by events into
+        # chunks of 20 steps (an event after every step would itself cost
+        # more than a step's launch overlap), per-step time of each chunk
+        chunk, n_chunks = 20, max(1, min(args.steps, 2000) // 20)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks + 1)]
+        evs[0].record(stream)
+        for c in range(n_chunks):
+            for i in range(c * chunk, (c + 1) * chunk):
+                step(i)
+            evs[c + 1].record(stream)
+        torch.cuda.synchronize()
+        per_step = np.array([evs[c].elapsed_time(evs[c + 1]) * 1e3 / chunk for c in range(n_chunks)])
 
         # (3) each kernel of the two-launch step alone, back to back
         def only_compute(i):
@@ -343,6 +355,12 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 6),
         "latency_us": round(lat_us, 3),
+        "latency_us_dist": {"p10": round(float(np.percentile(per_step, 10)), 3),
+                            "p50": round(float(np.percentile(per_step, 50)), 3),
+                            "p90": round(float(np.percentile(per_step, 90)), 3),
+                            "max": round(float(per_step.max()), 3), "chunks": int(n_chunks),
+                            "note": f"per-step time of each run of {chunk} consecutive steps of a back-to-back "
+                                    "loop (HIP events on the bench stream between the runs)"},
         "hbm_gbs_step": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
         "higher_is_better": True,
         "scaling": "weak",
