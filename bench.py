@@ -493,7 +493,7 @@ def measured_traffic(workload: str, kernel: str):
     since the counters were taken."""
     tag = {"arithmetic": "arithmetic_c1", "json": "json_c2", "schema": "schema_c3", "pylike": "pylike_c4",
            "stress": "stress_c5"}.get(workload, workload)
-    path = os.path.join(ROOT, "profiles", f"{tag}_pmc_traffic.md")
+    path = os.path.join(ROOT, "profiles", f"mask_kernels_{tag}_pmc_traffic.md")
     if not os.path.exists(path):
         return None
     meta = None
