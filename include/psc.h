@@ -41,8 +41,9 @@ typedef enum {
     PSC_E_NOT_BOUND = -6,   /* device tables not bound (psc_bind_device)              */
     PSC_E_LIMIT = -7,       /* the construction exceeded a size limit                 */
     PSC_E_IO = -8,          /* a file could not be opened, read or written            */
-    PSC_E_FORMAT = -9       /* not a classifier file, unsupported version, corrupt or
+    PSC_E_FORMAT = -9,      /* not a classifier file, unsupported version, corrupt or
                                inconsistent contents                                    */
+    PSC_E_NOT_VIABLE = -10  /* psc_host_state: the text has a lexical or syntax error  */
 } psc_status;
 
 typedef enum { PSC_F32 = 0, PSC_BF16 = 1 } psc_dtype;
@@ -363,6 +364,26 @@ psc_status psc_classify_host(const psc_handle *h, const int32_t *stacks, const i
 
 /* Copy class c's mask row (W words) to host memory. */
 psc_status psc_class_mask_host(const psc_handle *h, int32_t cls, uint32_t *out_row);
+
+/*
+ * The prefix state of a text (Sec. 3.2: the lexer state plus the LR parser
+ * stack after the text), computed on the host from the handle's lexer and
+ * parser tables, for callers that start decoding from a prompt or a partial
+ * output: its (q, stack) is what psc_compute_masks and the device states
+ * take.  The text (`len` bytes, host memory) is lexed from q0 by longest
+ * match with one byte of lookahead; every finished lexeme whose terminal is
+ * not ignored is fed to the parser (its reductions, then its shift); the
+ * last lexeme stays pending in *q.  The stack, s0 first, goes to `stack`
+ * (cap int32, host memory), its length to *stack_len.  Whether the pending
+ * lexeme can still complete is not checked: that is what the mask answers.
+ * Errors: PSC_E_INVALID_ARG (null pointers, cap < 1), PSC_E_NOT_VIABLE (a
+ * byte that no lexeme can take, or a terminal the parser rejects; the
+ * outputs are then unspecified), PSC_E_LIMIT (the stack would exceed cap),
+ * PSC_E_GRAMMAR (reductions that never end, only on corrupt tables).  Not
+ * used by any device call.
+ */
+psc_status psc_host_state(const psc_handle *h, const uint8_t *text, size_t len, int32_t *q, int32_t *stack,
+                          int32_t cap, int32_t *stack_len);
 
 /* Release the handle and its host tables (never the caller's device buffer). */
 void psc_free(psc_handle *h);

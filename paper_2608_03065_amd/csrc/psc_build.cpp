@@ -1418,6 +1418,77 @@ extern "C" psc_status psc_class_mask_host(const psc_handle *h, int32_t cls, uint
     return PSC_OK;
 }
 
+extern "C" psc_status psc_host_state(const psc_handle *h, const uint8_t *text, size_t len, int32_t *q,
+                                     int32_t *stack, int32_t cap, int32_t *stack_len) {
+    if (!h || (len > 0 && !text) || !q || !stack || !stack_len || cap < 1) {
+        set_error("psc_host_state: null argument or cap < 1");
+        return PSC_E_INVALID_ARG;
+    }
+    const AdvanceLayout &L = h->adv;
+    const int32_t *g = h->gram.data();
+    const int32_t *lex_next = g + L.lex_next, *lex_accept = g + L.lex_accept, *ignored = g + L.ignored;
+    const int32_t *action = g + L.action, *go = g + L.go, *prod_lhs = g + L.prod_lhs, *prod_len = g + L.prod_len;
+    int32_t n = 0;
+    auto push = [&](int32_t s) {
+        if (n >= cap) return false;
+        stack[n++] = s;
+        return true;
+    };
+    // more reductions than this for one terminal means the tables loop
+    const int64_t max_steps = (int64_t)(L.n_nt + 2) * (2 * (int64_t)cap + 8) + 65536;
+    // one terminal: the reductions its lookahead selects, then its shift
+    auto feed = [&](int32_t t) -> psc_status {
+        for (int64_t k = 0; k < max_steps; k++) {
+            const int32_t a = action[(int64_t)stack[n - 1] * L.n_term + t];
+            switch (a & 3) {
+            case 1:
+                return push(a >> 2) ? PSC_OK : PSC_E_LIMIT;
+            case 2: {
+                const int32_t p = a >> 2;
+                if (prod_len[p] >= n) return PSC_E_NOT_VIABLE;
+                n -= prod_len[p];
+                const int32_t s = go[(int64_t)stack[n - 1] * L.n_nt + prod_lhs[p]];
+                if (s < 0) return PSC_E_NOT_VIABLE;
+                if (!push(s)) return PSC_E_LIMIT;
+                break;
+            }
+            default:   // an error entry (accept is only ever reached with $end, never fed here)
+                return PSC_E_NOT_VIABLE;
+            }
+        }
+        return PSC_E_GRAMMAR;
+    };
+    push(0);                     // s0, the parser's start state
+    int32_t cur = 0;             // q0: nothing pending
+    psc_status st = PSC_OK;
+    for (size_t i = 0; i < len && st == PSC_OK; i++) {
+        const uint8_t c = text[i];
+        const int32_t nx = lex_next[(int64_t)cur * 256 + c];
+        if (nx >= 0) {
+            cur = nx;
+            continue;
+        }
+        // the pending lexeme ends here: it must be a terminal, and c starts the next one
+        const int32_t t = cur != 0 ? lex_accept[cur] : -1;
+        if (t < 0) {
+            st = PSC_E_NOT_VIABLE;
+            break;
+        }
+        if (!ignored[t]) st = feed(t);
+        cur = lex_next[c];
+        if (st == PSC_OK && cur < 0) st = PSC_E_NOT_VIABLE;
+    }
+    if (st != PSC_OK) {
+        set_error(st == PSC_E_NOT_VIABLE ? "psc_host_state: the text is not a viable prefix"
+                  : st == PSC_E_LIMIT    ? "psc_host_state: the stack would exceed cap"
+                                         : "psc_host_state: the parser tables loop");
+        return st;
+    }
+    *q = cur;
+    *stack_len = n;
+    return PSC_OK;
+}
+
 extern "C" void psc_free(psc_handle *h) { delete h; }
 
 extern "C" const char *psc_last_error(void) { return g_last_error.c_str(); }

@@ -17,14 +17,15 @@ LIB_PATH = os.path.join(_HERE, "libpsc.so")
 PSC_F32, PSC_BF16 = 0, 1
 ADV_OK, ADV_REJECTED, ADV_EOS, ADV_OVERFLOW, ADV_BAD_INPUT, ADV_SKIPPED = range(6)
 _STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E_OOM",
-           -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT", -8: "PSC_E_IO", -9: "PSC_E_FORMAT"}
+           -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT", -8: "PSC_E_IO", -9: "PSC_E_FORMAT",
+           -10: "PSC_E_NOT_VIABLE"}
 
 EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc_compute_masks",
             "psc_apply_mask", "psc_compute_and_apply", "psc_state_reset", "psc_advance",
             "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_compute_and_argmax",
             "psc_compute_and_argmax_dense", "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step",
             "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
-            "psc_free", "psc_last_error"]
+            "psc_host_state", "psc_free", "psc_last_error"]
 
 
 class PscError(RuntimeError):
@@ -177,6 +178,7 @@ def lib() -> C.CDLL:
         L.psc_device_error_count.argtypes = [P, P, I32, P]
         L.psc_classify_host.argtypes = [P, P, P, P, I32, P]
         L.psc_class_mask_host.argtypes = [P, I32, P]
+        L.psc_host_state.argtypes = [P, C.c_char_p, C.c_size_t, P, P, I32, P]
         L.psc_free.argtypes = [P]
         L.psc_free.restype = None
         L.psc_last_error.restype = C.c_char_p
@@ -184,7 +186,7 @@ def lib() -> C.CDLL:
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
                      "psc_compute_and_apply_dense", "psc_compute_and_argmax", "psc_compute_and_argmax_dense",
                      "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step", "psc_save", "psc_load", "psc_device_error_count",
-                     "psc_classify_host", "psc_class_mask_host"):
+                     "psc_classify_host", "psc_class_mask_host", "psc_host_state"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -286,6 +288,15 @@ class Classifier:
         row = np.zeros(self.W, np.uint32)
         _check(lib().psc_class_mask_host(self._h, int(cls), row.ctypes.data))
         return row
+
+    def host_state(self, text: bytes, cap: int = 1 << 16):
+        """psc_host_state: the prefix state (q, stack bottom->top) of `text`."""
+        _require(isinstance(text, (bytes, bytearray)), "text as bytes")
+        stack = np.zeros(max(int(cap), 1), np.int32)
+        q, n = C.c_int32(0), C.c_int32(0)
+        _check(lib().psc_host_state(self._h, bytes(text), len(text), C.byref(q), stack.ctypes.data, len(stack),
+                                    C.byref(n)))
+        return int(q.value), stack[:n.value].copy()
 
     def masks_host(self, states) -> np.ndarray:
         """Host walk + mask lookup (triage; not a device path)."""

@@ -212,3 +212,58 @@ def test_build_reports_out_of_memory():
                        env=env, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     assert "STATUS -4" in r.stdout and "AFTER 12" in r.stdout, r.stdout
+
+
+@pytest.mark.parametrize("name,steps", [("arithmetic", 200), ("json", 40), ("schema", 4)])
+def test_host_state_matches_input_side_parser(name, steps):
+    """psc_host_state on the workloads' prefixes equals the input side's own
+    host parser (inputs/hoststate.c), state for state."""
+    wl = configs.get(name)
+    clf = Classifier(wl.grammar, wl.vocab)
+    for s in range(steps):
+        for b in range(wl.B):
+            text = wl.prefix(s, b)
+            q, st = clf.host_state(text)
+            q2, st2 = wl.host.state(text)
+            assert q == q2 and np.array_equal(st, st2), (s, b, text[-40:])
+
+
+def test_host_state_matches_oracle_advance():
+    """Along greedily tokenised documents, the oracle's one-token advance
+    (Sec. 3.2) from the empty prefix reaches, after every token, the state
+    psc_host_state computes for the text so far."""
+    from inputs.seeds import rng_for
+    from recognizers import greedy_tokenize
+    wl = configs.get("json")
+    clf = Classifier(wl.grammar, wl.vocab)
+    orc = Oracle(wl.grammar, wl.vocab)
+    rng = rng_for(wl.index, salt=0x4057)
+    for _ in range(4):
+        doc = wl.make_document(rng, wl)
+        st = (0, np.array([0], np.int32))
+        text = b""
+        for tok in greedy_tokenize(doc, wl.vocab.tokens, wl.vocab.eos_id):
+            code, st = orc.advance(st, tok)
+            assert code == Oracle.ADVANCED
+            text += wl.vocab.tokens[tok]
+            q, stack = clf.host_state(text)
+            assert q == st[0] and np.array_equal(stack, st[1]), text[-40:]
+
+
+def test_host_state_errors():
+    wl = configs.get("arithmetic")
+    clf = Classifier(wl.grammar, wl.vocab)
+    q, st = clf.host_state(b"")
+    assert q == 0 and st.tolist() == [0]
+    # the last lexeme stays pending and is not fed: "1+)" is a prefix state
+    # (whose mask is empty), "1+)1" feeds the ")" and fails
+    assert clf.host_state(b"1+)")[1].size == 3
+    for bad in (b"1+)1", b"()1", b"1 2 ", b"a", b"1+a"):
+        with pytest.raises(PscError) as e:
+            clf.host_state(bad)
+        assert e.value.status == -10, bad
+    with pytest.raises(PscError) as e:
+        clf.host_state(b"((((((((((1", cap=4)
+    assert e.value.status == -7
+    with pytest.raises(ValueError):
+        clf.host_state("1+2")
