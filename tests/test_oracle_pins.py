@@ -171,3 +171,49 @@ def test_token_bits_agree_with_full_masks():
     rng = np.random.default_rng(5)
     toks = rng.integers(0, wl.V, size=2000)
     assert np.array_equal(o.token_bits(st, toks), full[toks])
+
+
+def _mutated(rng, doc: bytes, alphabet: bytes) -> bytes:
+    b = bytearray(doc)
+    for _ in range(int(rng.integers(1, 4))):
+        op, i = int(rng.integers(3)), int(rng.integers(0, len(b) + 1))
+        ch = alphabet[int(rng.integers(len(alphabet)))]
+        if op == 0 and len(b):
+            del b[min(i, len(b) - 1)]
+        elif op == 1:
+            b[i:i] = bytes([ch])
+        elif len(b):
+            b[min(i, len(b) - 1)] = ch
+    return bytes(b)
+
+
+@pytest.mark.parametrize("name,n_docs", [("arithmetic", 150), ("json", 12)])
+def test_teacher_forcing_rejects_negative_samples(name, n_docs):
+    """The RQ1 method's other half (Sec. 4.2): an invalid document, fed token
+    by token (greedy tokenisation) and then EOS, is rejected at some step.
+    Documents are mutated copies of valid ones, kept when the independent
+    recogniser says they are not in the language.  The oracle's masks and
+    the classifier's host walk decide every step identically."""
+    from paper_2608_03065_amd.psc import Classifier
+    wl = configs.get(name)
+    accepts = arith_accepts if name == "arithmetic" else json_accepts
+    alphabet = b"0123456789+*() " if name == "arithmetic" else b'{}[],:"\\ 0123456789.eE-+tfnaulrsx\x01'
+    o = Oracle(wl.grammar, wl.vocab)
+    clf = Classifier(wl.grammar, wl.vocab)
+    rng = rng_for(wl.index, salt=0xBAD)
+    negatives = 0
+    while negatives < n_docs:
+        doc = _mutated(rng, wl.make_document(rng, wl), alphabet)
+        if accepts(doc):
+            continue
+        negatives += 1
+        st, rejected = (0, np.array([0], np.int32)), False
+        for tok in greedy_tokenize(doc, wl.vocab.tokens, wl.vocab.eos_id) + [wl.vocab.eos_id]:
+            row = o.masks([st])[0]
+            assert np.array_equal(clf.masks_host([st])[0], row), doc
+            if not unpack(row, wl.V)[tok]:
+                rejected = True
+                break
+            code, st = o.advance(st, tok)
+            assert code == Oracle.ADVANCED, doc
+        assert rejected, doc
