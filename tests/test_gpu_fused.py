@@ -134,3 +134,27 @@ def test_fused_argument_errors(built):
     e0 = torch.zeros(0, dtype=torch.int32, device=DEV)
     clf.compute_and_apply(z, e0, e0, torch.zeros((0, wl.V), dtype=torch.float32, device=DEV))
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name,offset", [("arithmetic", 0), ("arithmetic", 1), ("json", 0), ("json", 1),
+                                         ("schema", 0), ("schema", 3)])
+def test_bitmask_rows_stay_in_bounds(built, name, offset):
+    """out_bitmask [B, W] placed `offset` words into a buffer filled with
+    canaries: compute_masks (16-byte and word-wise row copies) and the fused
+    step write exactly the B x W words, equal to the oracle's masks."""
+    wl, clf, orc = built(name)
+    states = wl.states(4)
+    want = orc.masks(states)
+    B, W = len(states), clf.W
+    stacks, lens, qs = pack_states(states, DEV)
+    for fused in (False, True):
+        buf = torch.full((offset + B * W + 67,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+        out = buf[offset:offset + B * W].view(B, W)
+        if fused:
+            lg = wl.logits(4).to(DEV)
+            clf.compute_and_apply(stacks, lens, qs, lg, out=out)
+        else:
+            clf.compute_masks(stacks, lens, qs, out=out)
+        h = buf.cpu().numpy()
+        assert (h[:offset] == 0x5A5A5A5A).all() and (h[offset + B * W:] == 0x5A5A5A5A).all(), fused
+        assert np.array_equal(h[offset:offset + B * W].view(np.uint32).reshape(B, W), want), fused
