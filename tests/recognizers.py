@@ -211,6 +211,134 @@ def json_accepts(s: bytes) -> bool:
     return p.i == len(s)
 
 
+class _End(Exception):
+    """The text ended where the document could still go on."""
+
+
+class _JPrefix:
+    """JSON read in prefix mode: running out of text anywhere a document
+    could continue means the text is a viable prefix."""
+
+    def __init__(self, s: bytes):
+        self.s = s
+        self.i = 0
+
+    def peek(self) -> int:
+        if self.i >= len(self.s):
+            raise _End
+        return self.s[self.i]
+
+    def ws(self):
+        while self.i < len(self.s) and self.s[self.i] in _WS:
+            self.i += 1
+
+    def lit(self, word: bytes) -> bool:
+        rest = self.s[self.i:self.i + len(word)]
+        if rest == word:
+            self.i += len(word)
+            return True
+        if len(rest) < len(word) and word.startswith(rest):
+            raise _End
+        return False
+
+    def string(self) -> bool:
+        if self.peek() != 0x22:
+            return False
+        self.i += 1
+        while True:
+            c = self.peek()
+            if c == 0x22:
+                self.i += 1
+                return True
+            if c < 0x20:
+                return False
+            self.i += 1
+            if c != 0x5C:
+                continue
+            e = self.peek()
+            self.i += 1
+            if e == 0x75:
+                for _ in range(4):
+                    if self.peek() not in _HEX:
+                        return False
+                    self.i += 1
+            elif e not in _ESC:
+                return False
+
+    def digits(self) -> int:
+        n = 0
+        while self.i < len(self.s) and 0x30 <= self.s[self.i] <= 0x39:
+            self.i += 1
+            n += 1
+        return n
+
+    def number(self) -> bool:
+        if self.peek() == 0x2D:
+            self.i += 1
+        c = self.peek()
+        if c == 0x30:
+            self.i += 1
+        elif 0x31 <= c <= 0x39:
+            self.digits()
+        else:
+            return False
+        if self.i < len(self.s) and self.s[self.i] == 0x2E:
+            self.i += 1
+            if self.digits() == 0:
+                self.peek()            # text ends after the point: more digits may come
+                return False
+        if self.i < len(self.s) and self.s[self.i] in b"eE":
+            self.i += 1
+            if self.peek() in b"+-":
+                self.i += 1
+            if self.digits() == 0:
+                self.peek()
+                return False
+        return True
+
+    def value(self) -> bool:
+        self.ws()
+        c = self.peek()
+        if c == 0x7B or c == 0x5B:
+            close = b"}" if c == 0x7B else b"]"
+            self.i += 1
+            self.ws()
+            if self.lit(close):
+                return True
+            while True:
+                if c == 0x7B:
+                    self.ws()
+                    if not self.string():
+                        return False
+                    self.ws()
+                    if not self.lit(b":"):
+                        return False
+                if not self.value():
+                    return False
+                self.ws()
+                if self.lit(close):
+                    return True
+                if not self.lit(b","):
+                    return False
+        if c == 0x22:
+            return self.string()
+        if c == 0x2D or 0x30 <= c <= 0x39:
+            return self.number()
+        return self.lit(b"true") or self.lit(b"false") or self.lit(b"null")
+
+
+def json_viable_prefix(s: bytes) -> bool:
+    """Is s the beginning of some JSON document (s itself included)?"""
+    p = _JPrefix(s)
+    try:
+        if not p.value():
+            return False
+        p.ws()
+        return p.i == len(s)
+    except _End:
+        return True
+
+
 def greedy_tokenize(text: bytes, tokens: list[bytes], eos_id: int) -> list[int]:
     """Longest-match tokenisation over a vocabulary (teacher forcing)."""
     from inputs.vocab import Vocab

@@ -74,6 +74,7 @@ BATTERY = [
     ("teacher_json", lambda: pins.test_teacher_forcing_never_rejects_the_true_token("json", 6)),
     ("eos_nonempty_json", lambda: pins.test_eos_iff_member_and_nonempty("json", 8)),
     ("closure_json", lambda: pins.test_prefix_closure("json", 4)),
+    ("prefix_language_json", pins.test_json_masks_equal_prefix_language),
     ("exhaustive_arith", pins.test_exhaustive_arithmetic_prefix_language),
 ]
 

@@ -217,3 +217,26 @@ def test_teacher_forcing_rejects_negative_samples(name, n_docs):
             code, st = o.advance(st, tok)
             assert code == Oracle.ADVANCED, doc
         assert rejected, doc
+
+
+def test_json_masks_equal_prefix_language():
+    """On the JSON workload, token v is allowed after x exactly when x v is
+    the beginning of some JSON document, decided by an independent
+    prefix-mode recogniser written from the JSON grammar; EOS exactly when
+    x is a document.  Every single-byte token and 1,500 random multi-byte
+    ones, after 48 prefixes of the workload (cut to at most 120 bytes)."""
+    from recognizers import json_viable_prefix
+    wl = configs.get("json")
+    o = Oracle(wl.grammar, wl.vocab)
+    toks = wl.vocab.tokens
+    rng = np.random.default_rng(0x150)
+    pick = np.unique(np.concatenate([[i for i, t in enumerate(toks) if len(t) == 1],
+                                     rng.integers(0, wl.V - 1, 1500)]))
+    prefixes = [wl.prefix(s, b)[:120] for s in range(3) for b in range(wl.B)]
+    masks = o.masks([wl.host.state(x) for x in prefixes])
+    for x, row in zip(prefixes, masks):
+        m = unpack(row, wl.V)
+        assert m[wl.vocab.eos_id] == json_accepts(x), x
+        want = np.array([json_viable_prefix(x + toks[i]) for i in pick])
+        bad = pick[m[pick] != want]
+        assert bad.size == 0, (x, [toks[i] for i in bad[:5]])
