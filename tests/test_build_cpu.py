@@ -188,7 +188,7 @@ wl = configs.get("schema")
 G, voc = wl.grammar, wl.vocab
 vm = int([l for l in open("/proc/self/status") if l.startswith("VmSize")][0].split()[1]) * 1024
 soft, hard = resource.getrlimit(resource.RLIMIT_AS)
-resource.setrlimit(resource.RLIMIT_AS, (vm + (64 << 20), hard))
+resource.setrlimit(resource.RLIMIT_AS, (vm + (16 << 20), hard))
 try:
     psc.Classifier(G, voc)
     print("BUILT", flush=True)
@@ -202,7 +202,7 @@ print("AFTER", psc.Classifier(a.grammar, a.vocab).info()["n_lr_states"], flush=T
 
 def test_build_reports_out_of_memory():
     """An allocation failure inside psc_build (forced with an address-space
-    limit of 64 MB above what the process holds, far below what the schema
+    limit of 16 MB above what the process holds, far below what the schema
     construction needs) is PSC_E_OOM, not a crash; the process then builds
     another classifier normally."""
     import subprocess
