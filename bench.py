@@ -47,6 +47,17 @@ def main():
                     help="tokens per sequence in the on-device decoding loop (advance + masks)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration under rocprofv3 --pmc)")
+    ap.add_argument("--masks", choices=["flat", "sliced"], default="flat",
+                    help="layout of the mask table on the device (psc_bind_device_ex)")
+    ap.add_argument("--predictor-batches", type=int, default=200,
+                    help="held-out prefix batches walked once before the warmup to fill the class predictor "
+                         "(0: start empty)")
+    ap.add_argument("--timeline", type=int, default=0,
+                    help="also run this many steps of the timeline variant and report per-workgroup times")
+    ap.add_argument("--speculate", action="store_true",
+                    help="PSC_OPT_SPECULATE: the fused step loads the predicted class's data during the walk")
+    ap.add_argument("--no-prequeue", action="store_true",
+                    help="time loops without first queueing them behind a device-side delay")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
@@ -72,7 +83,8 @@ def main():
     log(f"psc_build {info['build_seconds']:.2f}s states={info['dfa_states']} classes={info['n_classes']}"
         f" (total setup {time.time() - t0:.1f}s)")
     stream = torch.cuda.Stream(device=dev)     # default priority
-    clf.bind(dev, stream=stream)
+    clf.bind(dev, stream=stream, layout=args.masks)
+    clf.set_options(speculate=args.speculate)
 
     n_distinct = args.distinct_steps or wl.steps
     n_distinct = max(1, min(n_distinct, wl.steps))
@@ -112,6 +124,41 @@ def main():
         del src_t, dst_t
         log(f"calibration copy: 3 x {args.calibration_copy_mb} MiB device-to-device")
 
+    # the class predictor, filled from prefix batches the timed steps do not
+    # use (the workload's generator at step indices past its own), as a
+    # decoding loop fills it from its first steps or a prompt set
+    t0 = time.time()
+    n_calib = 0
+    with torch.cuda.stream(stream):
+        for s_ in range(args.predictor_batches):
+            st_, ln_, q_ = pack_states(wl.states(wl.steps + s_), dev)
+            clf.compute_classes(st_, ln_, q_, stream=stream)
+            n_calib += B
+    torch.cuda.synchronize()
+    calib_updates = clf.predictor_updates(reset=True, stream=stream)
+    log(f"class predictor: {args.predictor_batches} held-out batches walked ({time.time() - t0:.1f}s), "
+        f"{calib_updates} entries set")
+
+    # a device-side delay in front of a timed loop lets the host queue the
+    # whole loop before the first event fires, so that the host's launch
+    # latency stays out of the timed region (the GPU time of the steps)
+    sleep_cycles_per_us = None
+
+    def prequeue(n_calls, us_per_call=12.0):
+        nonlocal sleep_cycles_per_us
+        if args.no_prequeue:
+            return
+        if sleep_cycles_per_us is None:
+            a_, z_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(1000)
+            a_.record(stream)
+            torch.cuda._sleep(1 << 20)
+            z_.record(stream)
+            torch.cuda.synchronize()
+            sleep_cycles_per_us = (1 << 20) / max(a_.elapsed_time(z_) * 1e3, 1.0)
+        want_us = min(100.0 + n_calls * us_per_call, 60000.0)
+        torch.cuda._sleep(int(want_us * sleep_cycles_per_us))
+
     def fused_step(i):
         stacks, lens, qs = step_inputs[i % n_distinct]
         clf.compute_and_apply(stacks, lens, qs, pool[i % n_pool], out=bms[i % n_bm], stream=stream)
@@ -131,6 +178,7 @@ def main():
         for i in range(warm):
             fn(i)
         torch.cuda.synchronize()
+        prequeue(n)
         a.record(stream)
         for i in range(n):
             fn(i)
@@ -144,7 +192,10 @@ def main():
         torch.cuda.synchronize()
 
         # (1) the timed loop: exactly --steps steps, whole-step latency
+        torch.cuda.synchronize()
+        clf.predictor_updates(reset=True, stream=stream)
         ms_per_step = loop(step, args.steps, warm=0) * 1e-3
+        timed_misses = clf.predictor_updates(reset=True, stream=stream)
         # (2) the other formulation of the same step, for comparison
         t_other = loop(other, min(args.steps, 1000))
         # (2b) the spread: the same back-to-back loop cut by events into
@@ -152,6 +203,8 @@ def main():
         # more than a step's launch overlap), per-step time of each chunk
         chunk, n_chunks = 20, max(1, min(args.steps, 2000) // 20)
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks + 1)]
+        torch.cuda.synchronize()
+        prequeue(n_chunks * chunk)
         evs[0].record(stream)
         for c in range(n_chunks):
             for i in range(c * chunk, (c + 1) * chunk):
@@ -274,6 +327,10 @@ def main():
         t_fill = graph_loop(fill)
         t_copy = graph_loop(copy)
 
+        tl = None
+        if args.timeline > 0:
+            tl = timeline(clf, wl, step_inputs, pool, bms, stream, dev, args.timeline, prequeue)
+
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
         # advanced by one token each (psc_advance), then the single-launch
         # step on them (psc_compute_and_apply_dense)
@@ -317,7 +374,7 @@ def main():
     achieved_apply = bytes_apply_solo / (t_apply * 1e-6) / 1e9
     fast = V % 32 == 0
     if args.mode == "fused":
-        kname = "fused_fast_kernel" if fast else "fused_generic_kernel"
+        kname = ("fused_spec_kernel" if args.speculate else "fused_fast_kernel") if fast else "fused_generic_kernel"
         achieved = bytes_fused / (lat_us * 1e-6) / 1e9
         roofline = {
             "bound": "hbm", "kernel": kname,
@@ -345,6 +402,23 @@ def main():
             "avg_launch_us": round(t_apply, 3),
             "timing": "HIP events around 1000 back-to-back launches of the kernel alone on the bench stream",
         }
+
+    # the two-call step of the boundary (psc_compute_masks, then
+    # psc_apply_mask on the same stream), measured as the other mode above
+    t_two = t_other if args.mode == "fused" else lat_us
+    ach_two = bytes_two_launch / (t_two * 1e-6) / 1e9
+    roofline_two = {
+        "calls": "psc_compute_masks + psc_apply_mask (two launches, one stream)",
+        "bound": "hbm", "kernels": ["walk_gather_kernel", "apply_fast_kernel" if fast else "apply_generic_kernel"],
+        "achieved": round(ach_two, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(ach_two / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_step": round(bytes_two_launch),
+        "step_us": round(t_two, 3),
+        "per_kernel_us": {"compute_masks": round(t_compute, 3), "apply_mask": round(t_apply, 3),
+                          "compute_masks_graph": round(t_compute_graph, 3),
+                          "apply_mask_graph": round(t_apply_graph, 3)},
+    }
+    if args.mode == "fused":
+        roofline["calls"] = "psc_compute_and_apply (one launch)"
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -401,6 +475,19 @@ def main():
                            "two_launch": round(bytes_two_launch),
                            "one_pass_read_write_model": round(one_pass_model)},
         "roofline": roofline,
+        "roofline_two_launch": roofline_two,
+        "predictor": {"held_out_batches": args.predictor_batches, "entries_set": calib_updates,
+                      "misses_in_timed_loop": timed_misses,
+                      "miss_rate_in_timed_loop": round(timed_misses / max(1, args.steps * B), 4),
+                      "note": "class predictor filled by psc_compute_classes over prefix batches the timed "
+                              "steps do not use; a miss is a walk whose class differed from the prediction "
+                              "(results never depend on it)"},
+        "mask_layout": args.masks,
+        "speculate": bool(args.speculate),
+        "timing_method": ("each timed loop is queued behind a device-side delay (torch.cuda._sleep) so that "
+                          "the host's launch latency is not in the timed region" if not args.no_prequeue else
+                          "loops launched eagerly from the host"),
+        "timeline": tl,
         "reference_kernels_us": {
             "torch_fill_logits": round(t_fill, 3), "torch_copy_logits": round(t_copy, 3),
             "fill_gbs": round(B * V * s_logit / (t_fill * 1e-6) / 1e9, 1),
@@ -408,10 +495,59 @@ def main():
             "note": "torch's fill_ and copy_ of one [B, V] logits tensor, 100 per HIP graph, replayed"},
         "cpu_baseline": cpu,
         "build": {k: info[k] for k in ("dfa_states_built", "dfa_states", "n_classes", "table_bytes",
-                                        "mask_table_bytes", "build_seconds", "dfa_rows", "dense_rows",
-                                        "chain_states", "chains")},
+                                        "mask_table_bytes", "sliced_mask_bytes", "mask_slices_unique",
+                                        "build_seconds", "dfa_rows", "dense_rows", "chain_states", "chains")},
     }
     print(json.dumps(out), flush=True)
+
+
+def timeline(clf, wl, step_inputs, pool, bms, stream, dev, n_steps, prequeue):
+    """n_steps back-to-back launches of the fused step's timeline variant
+    (psc_compute_and_apply_timeline): per wavefront the GPU's 100 MHz clock
+    at its start, after the walk's first step, when the class is known and
+    after its last store.  Returns percentiles in microseconds, relative to
+    the earliest start in each launch."""
+    import numpy as np
+    import torch
+    B = wl.B
+    tdt = pool[0].dtype
+    n = clf.timeline_records(B, tdt)
+    recs = torch.zeros((n_steps, n, 4), dtype=torch.int64, device=dev)
+    n_distinct, n_pool, n_bm = len(step_inputs), len(pool), len(bms)
+    torch.cuda.synchronize()
+    prequeue(n_steps)
+    for i in range(n_steps):
+        st, ln, q = step_inputs[i % n_distinct]
+        clf.compute_and_apply_timeline(st, ln, q, pool[i % n_pool], recs[i], out=bms[i % n_bm], stream=stream)
+    torch.cuda.synchronize()
+    r = recs.cpu().numpy().view(np.uint64).astype(np.int64)
+    t0 = r[:, :, 0]
+    tA, tB = t0 + (r[:, :, 1] & 0xFFFFFFFF), t0 + (r[:, :, 1] >> 32)
+    tE, meta = t0 + (r[:, :, 2] & 0xFFFFFFFF), r[:, :, 2] >> 32
+    wave, held, done = meta & 7, (meta >> 7) & 1, (meta >> 8) & 1
+    start = t0.min(axis=1, keepdims=True)
+    us = lambda x: x * 0.01                     # 100 MHz ticks
+
+    def pct(x):
+        return {k: round(float(v), 3) for k, v in zip(("p10", "p50", "p90", "max"),
+                                                          np.percentile(x, [10, 50, 90, 100]))}
+    walker, worker = wave == 0, wave > 0
+    end = tE.max(axis=1)
+    gaps = us(start[1:, 0] - end[:-1]) if n_steps > 1 else np.zeros(1)
+    return {
+        "steps": n_steps, "records_per_step": int(n),
+        "wavefront_start_us": pct(us(t0 - start)[worker]),
+        "prediction_known_us": pct(us(tA - start)[walker]),
+        "class_known_us": pct(us(tB - start)[walker]),
+        "last_store_issued_us": pct(us(tE - start)[worker]),
+        "launch_span_us": pct(us(end - start[:, 0])),
+        "gap_to_next_launch_us": pct(gaps),
+        "walks_ended_at_first_step": round(float(done[walker].mean()), 4),
+        "prediction_held": round(float(held[walker & (done == 0)].mean()) if (walker & (done == 0)).any() else 0.0,
+                                 4),
+        "note": "times from the earliest wavefront start of each launch; walker = wavefront 0 of a workgroup, "
+                "workers = the wavefronts that move the data",
+    }
 
 
 def decode_steps(wl, clf, B, pool, bms, stream, dev, max_steps):

@@ -114,7 +114,23 @@ typedef struct {
     double build_seconds;      /* wall time of psc_build                      */
     int32_t chain_states;      /* walked states stored as chain entries       */
     int32_t chains;            /* chains they form                            */
+    int32_t mask_slices_unique; /* distinct 64-word slices of the mask rows   */
+    int32_t bound_mask_layout; /* 0 unbound, PSC_BIND_FLAT or PSC_BIND_SLICED */
+    int64_t sliced_mask_bytes; /* the mask table in the sliced layout: the
+                                  distinct slices plus a slice id per row and
+                                  slice (compare mask_table_bytes)            */
 } psc_info_t;
+
+/* Layouts of the mask table in the bound buffer (psc_bind_device_ex).
+ *  PSC_BIND_FLAT    every class's row stored whole: one dependent load per
+ *                   mask word after the class is known.
+ *  PSC_BIND_SLICED  each row cut into 64-word slices and every distinct slice
+ *                   stored once, with a slice id per (row, slice): the
+ *                   runtime form of the precomputed masks compressed (the
+ *                   paper's runtime mask memory, Tab. runtime_overhead), at
+ *                   the cost of a second dependent load per mask word.
+ * Every call gives bit-identical results under either layout. */
+enum { PSC_BIND_FLAT = 1, PSC_BIND_SLICED = 2 };
 
 /*
  * Offline construction (Algorithm 1; Sec. 3.1-3.5), CPU only.  Lexes every
@@ -153,6 +169,10 @@ psc_status psc_info(const psc_handle *h, psc_info_t *out);
 /* Device bytes psc_bind_device needs (256-byte aligned buffer). */
 size_t psc_device_bytes(const psc_handle *h);
 
+/* Device bytes psc_bind_device_ex needs for the mask layout in `flags`
+ * (PSC_BIND_FLAT, PSC_BIND_SLICED, or 0 for the default layout). */
+size_t psc_device_bytes_ex(const psc_handle *h, uint32_t flags);
+
 /*
  * Copy the classifier and mask tables, and the lexer, parser and vocabulary
  * that psc_advance reads, into caller-allocated device memory (dev_buf,
@@ -163,6 +183,12 @@ size_t psc_device_bytes(const psc_handle *h);
  * PSC_E_OOM (the tables derived at bind time do not fit in host memory).
  */
 psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream);
+
+/* psc_bind_device with the mask table in the layout `flags` selects
+ * (PSC_BIND_FLAT or PSC_BIND_SLICED; 0 = the default, PSC_BIND_FLAT);
+ * nbytes >= psc_device_bytes_ex(h, flags).  Also clears the class predictor
+ * (psc_predictor_fill) and the device counters. */
+psc_status psc_bind_device_ex(psc_handle *h, void *dev_buf, size_t nbytes, uint32_t flags, void *stream);
 
 /*
  * Per-step mask computation (Algorithm 2, classification and mask steps).
@@ -190,6 +216,19 @@ psc_status psc_compute_masks(const psc_handle *h, const int32_t *stacks, const i
                              void *stream);
 
 /*
+ * The ragged-stack calls (psc_compute_masks, psc_compute_classes,
+ * psc_compute_and_apply, psc_compute_and_argmax) trust the device lengths to
+ * fit `stacks`.  Their *_n forms take n_stack, the number of int32 symbols
+ * the caller's `stacks` buffer holds (>= 0): a sequence whose stack would
+ * reach past it (offset + length > n_stack) is a rejected input (all-zero
+ * row, or -1, and a count in the error counter) and is never read.
+ * Otherwise identical to the calls without _n.
+ */
+psc_status psc_compute_masks_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                               const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                               uint32_t *out_bitmask, void *stream);
+
+/*
  * Mask application (Sec. 1, Fig. 1a: logits are masked before sampling), in
  * place on a contiguous device tensor logits[B][V] of `dtype`:
  *   logits[b][v] = -inf   wherever bit v of bitmask[b] (uint32 [B][ceil(V/32)]) is 0;
@@ -212,6 +251,9 @@ psc_status psc_apply_mask(void *logits, psc_dtype dtype, const uint32_t *bitmask
  */
 psc_status psc_compute_classes(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                const int32_t *lexer_states, int32_t B, int32_t *out_classes, void *stream);
+psc_status psc_compute_classes_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                 const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                 int32_t *out_classes, void *stream);
 
 /*
  * The whole per-step path in one launch: psc_compute_masks followed by
@@ -232,6 +274,69 @@ psc_status psc_compute_classes(const psc_handle *h, const int32_t *stacks, const
 psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                  const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
                                  psc_dtype dtype, int32_t V, void *stream);
+psc_status psc_compute_and_apply_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                   const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                   uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                   void *stream);
+
+/*
+ * The class predictor.  A walk's first step from start[q] leaves the start
+ * block of lexer state q in one of a few ways (which edge, or how far along
+ * a chain); psc_compute_and_apply, psc_compute_masks and psc_compute_classes
+ * record, per such (q, way), the class the walk then reached.  When a later
+ * walk leaves the same way, the workgroups of psc_compute_and_apply and
+ * psc_compute_masks start loading that class's mask words (and the logits it
+ * leaves partly allowed) while the walk goes on, and use them if the walk
+ * ends in that class; otherwise they load the right ones.  The predictor
+ * only decides what is loaded early, never a result: every output is the
+ * same whatever it holds.  It lives in the bound buffer; concurrent calls on
+ * one handle may overwrite each other's entries, which is harmless.
+ * psc_compute_classes over sample prefix states (e.g. a prompt set) fills it
+ * before decoding starts.
+ *
+ * psc_predictor_fill sets every entry to `cls` (-1: no prediction; else a
+ * class id < n_classes), on `stream`.  psc_predictor_updates reads
+ * (synchronously) the number of entries the calls above have changed since
+ * the last reset, i.e. walks whose class differed from the prediction, and
+ * optionally resets it.  Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND,
+ * PSC_E_DEVICE.
+ */
+psc_status psc_predictor_fill(const psc_handle *h, int32_t cls, void *stream);
+
+/*
+ * Options of a handle's device calls (a bitwise OR; 0 = the defaults):
+ *  PSC_OPT_SPECULATE  psc_compute_and_apply loads the predicted class's mask
+ *                     words and partly allowed logits during the walk (the
+ *                     class predictor above); results are identical either
+ *                     way.  Off by default: on MI355X the walk's loads and
+ *                     the workgroup's second barrier cost about what the
+ *                     early loads save.
+ * Errors: PSC_E_INVALID_ARG (null handle, unknown option).
+ */
+enum { PSC_OPT_SPECULATE = 1 };
+psc_status psc_set_options(psc_handle *h, uint32_t options);
+psc_status psc_predictor_updates(const psc_handle *h, uint32_t *out, int32_t reset, void *stream);
+
+/*
+ * psc_compute_and_apply_n with a per-wavefront timeline for profiling: every
+ * wavefront of the launch writes one record of four uint64 to `records`
+ * (device memory, n_records >= psc_timeline_records(h, B, dtype)), in the
+ * order (sequence, slice, wavefront).  Times are ticks of the GPU's constant
+ * 100 MHz clock:
+ *   [0] its start;
+ *   [1] (after the walk's first step, with PSC_OPT_SPECULATE; else = start)
+ *       - start, then (its class known) - start << 32;
+ *   [2] (its last store issued) - start, then, << 32: wavefront | XCD << 3 |
+ *       prediction held << 7 | class known at the first step << 8;
+ *   [3] sequence | slice << 32.
+ * Results are those of psc_compute_and_apply_n.  Fast path only
+ * (V % 32 == 0, 16-byte aligned logits): PSC_E_INVALID_ARG otherwise.
+ */
+int64_t psc_timeline_records(const psc_handle *h, int32_t B, psc_dtype dtype);
+psc_status psc_compute_and_apply_timeline(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                          uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                          uint64_t *records, int64_t n_records, void *stream);
 
 /*
  * Greedy decoding folded into the mask step (the mask decides which logits
@@ -250,6 +355,10 @@ psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, con
 psc_status psc_compute_and_argmax(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                   const int32_t *lexer_states, int32_t B, const void *logits, psc_dtype dtype,
                                   int32_t V, int32_t *out_tokens, void *stream);
+psc_status psc_compute_and_argmax_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                    const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                    const void *logits, psc_dtype dtype, int32_t V, int32_t *out_tokens,
+                                    void *stream);
 
 /*
  * Device-resident prefix states (Sec. 3.2: a prefix is represented by its

@@ -915,14 +915,71 @@ psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string 
 
 using namespace psc;
 
-size_t psc_handle::device_bytes_needed() const {
-    auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
-    return psc::table_off(n_lex) + up(table.size() * sizeof(int32_t)) + up(masks.size() * sizeof(uint32_t)) +
-           up(gram.size() * sizeof(int32_t)) + up(vbytes.size()) + kArgmaxBytes +
-           up((size_t)n_lr * adv.n_term * sizeof(int32_t)) + up(psc::goto_closure_bytes(*this));
-}
+size_t psc_handle::device_bytes_needed(uint32_t flags) const { return psc::device_layout(*this, flags).total; }
 
 namespace psc {
+DeviceLayout device_layout(const psc_handle &h, uint32_t flags) {
+    auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
+    DeviceLayout L{};
+    L.sliced = (flags & PSC_BIND_SLICED) != 0;
+    L.table = table_off(h.n_lex);
+    L.masks = L.table + up(h.table.size() * sizeof(int32_t));
+    if (L.sliced) {
+        L.ids = L.masks + up(h.slices.size() * sizeof(uint32_t));
+        L.gram = L.ids + up(h.slice_ids.size() * sizeof(int32_t));
+    } else {
+        L.ids = L.masks;
+        L.gram = L.masks + up(h.masks.size() * sizeof(uint32_t));
+    }
+    L.vbytes = L.gram + up(h.gram.size() * sizeof(int32_t));
+    L.argmax = L.vbytes + up(h.vbytes.size());
+    L.packed = L.argmax + kArgmaxBytes;
+    L.closure = L.packed + up((size_t)h.n_lr * h.adv.n_term * sizeof(int32_t));
+    L.pred = L.closure + up(goto_closure_bytes(h));
+    L.total = L.pred + up((size_t)start_block_count(h.n_lex) * kPredInts * sizeof(int32_t));
+    return L;
+}
+
+void slice_masks(psc_handle &h) {
+    const int64_t nc = h.n_classes;
+    const int32_t ns = h.mask_stride / kSliceWords;
+    h.n_slices = ns;
+    h.slice_ids.assign((size_t)nc * ns, 0);
+    h.slices.clear();
+    // open addressing over the distinct slices, keyed by a 64-bit hash
+    size_t cap = 1024;   // a power of two, at least twice the number of slices
+    while (cap < (size_t)(nc * ns) * 2) cap <<= 1;
+    std::vector<int32_t> slot(cap, -1);
+    std::vector<uint64_t> key(cap, 0);
+    int32_t n = 0;
+    for (int64_t c = 0; c < nc; c++)
+        for (int32_t k = 0; k < ns; k++) {
+            const uint32_t *w = h.masks.data() + (size_t)c * h.mask_stride + (size_t)k * kSliceWords;
+            uint64_t x = 0x9E3779B97F4A7C15ull;
+            for (int i = 0; i < kSliceWords; i++) x = mix64(x ^ w[i]);
+            size_t at = (size_t)x & (cap - 1);
+            int32_t id = -1;
+            for (;; at = (at + 1) & (cap - 1)) {
+                if (slot[at] < 0) break;
+                if (key[at] == x &&
+                    std::equal(w, w + kSliceWords, h.slices.data() + (size_t)slot[at] * kSliceWords)) {
+                    id = slot[at];
+                    break;
+                }
+            }
+            if (id < 0) {
+                id = n++;
+                slot[at] = id;
+                key[at] = x;
+                h.slices.insert(h.slices.end(), w, w + kSliceWords);
+            }
+            h.slice_ids[(size_t)c * ns + k] = id;
+        }
+    h.n_unique_slices = n;
+    h.info.mask_slices_unique = n;
+    h.info.sliced_mask_bytes = (int64_t)(h.slices.size() + h.slice_ids.size()) * 4;
+}
+
 bool packed_action(const psc_handle &h, std::vector<int32_t> &out) {
     out.clear();
     const AdvanceLayout &L = h.adv;
@@ -1329,6 +1386,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         I.chains = (int32_t)chains.size();
         I.table_bytes = (int64_t)h->table.size() * 4;
         I.mask_table_bytes = (int64_t)h->masks.size() * 4;
+        slice_masks(*h);
         I.device_bytes = (int64_t)h->device_bytes_needed();
         I.build_seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
         *out = owned.release();
@@ -1357,6 +1415,10 @@ extern "C" psc_status psc_info(const psc_handle *h, psc_info_t *out) {
 }
 
 extern "C" size_t psc_device_bytes(const psc_handle *h) { return h ? h->device_bytes_needed() : 0; }
+
+extern "C" size_t psc_device_bytes_ex(const psc_handle *h, uint32_t flags) {
+    return h ? h->device_bytes_needed(flags) : 0;
+}
 
 extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                         const int32_t *lexer_states, int32_t B, int32_t *out_classes) {

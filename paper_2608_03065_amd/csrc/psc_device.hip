@@ -1,8 +1,10 @@
 // Device side of the mask library (gfx950): table binding, the classifier
 // walk + mask gather (Algorithm 2, classification and mask steps), the
-// in-place bitmask -> logits application, the fused single-launch step, the
-// masked argmax, and the lexing and parsing steps on device-resident prefix
-// states (the advance, and the whole decoding step in one launch).
+// in-place bitmask -> logits application, the fused single-launch step (and
+// its speculative form and profiling timeline), the masked argmax, and the
+// lexing and parsing steps on device-resident prefix states (the advance,
+// and the whole decoding step in one launch).  The mask table is read in
+// either layout (flat, or deduplicated 64-word slices): kSliced below.
 //
 // Nothing here is a dense contraction, so no matrix cores are used; the walk
 // and the advance are chains of dependent table loads (latency-bound) and
@@ -107,7 +109,7 @@ constexpr int32_t kRefFault = INT32_MIN;   // no class ref is this small
 
 // With kOverlay, stack indices >= ptr are read from `ov` (the states a
 // token pushed, in LDS, not yet written to memory) instead of `st`.
-template <bool kOverlay = false>
+template <bool kOverlay = false, bool kTrack = false>
 struct Walk {
     const int32_t *__restrict__ table;
     const int32_t *__restrict__ st;
@@ -120,6 +122,11 @@ struct Walk {
     int cls;          // the result once the walk has ended
     const int32_t *ov = nullptr;
     int ptr = 0;
+    // kTrack: how the last step left its wavefront load -- the lane (sparse
+    // row: the matched edge's, or lane 1 for the default; chain: the entry
+    // the walk left by) and the kind (0: a sparse edge or a chain entry's
+    // second edge; 1: a default or the chain's end); the class predictor's key
+    int exit_lane = -1, exit_kind = 0;
 
     __device__ __forceinline__ int load(int idx) const {
         if (kOverlay && idx >= ptr) return ov[idx - ptr];
@@ -139,6 +146,10 @@ struct Walk {
         // lane 63 never passes (src >= kChunk), so f <= 63
         const int f = __ffsll((long long)__ballot(!pass)) - 1;
         const int fx = __builtin_amdgcn_readlane(e.x, f);
+        if (kTrack) {
+            exit_lane = f;
+            exit_kind = 1;
+        }
         if ((fx & 0xFFFF) == kSymJump) {          // end of the chain: go on without reading
             i -= f;
             ref = __builtin_amdgcn_readlane(e.z, f);
@@ -153,6 +164,7 @@ struct Walk {
         const int fX = __builtin_amdgcn_readlane(Xl, f);
         if (fX < 0 || fX >= n_lr) { cls = -1; return true; }
         i -= f + 1;
+        if (kTrack) exit_kind = fX == (int)((uint32_t)fx >> 16) ? 0 : 1;
         ref = fX == (int)((uint32_t)fx >> 16) ? __builtin_amdgcn_readlane(e.y, f)
                                               : __builtin_amdgcn_readlane(e.z, f);
         return false;
@@ -167,6 +179,10 @@ struct Walk {
         const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
         const int nref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
                              : __builtin_amdgcn_readlane(va, 1);
+        if (kTrack) {
+            exit_lane = hit ? __ffsll((long long)hit) - 1 : 1;
+            exit_kind = 0;
+        }
         // a symbol out of range ends the walk through kRefFault; a select,
         // not a branch, so that the row load cannot sink below the window
         ref = X >= 0 && X < n_lr ? nref : kRefFault;
@@ -246,6 +262,72 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
     }
 }
 
+// A walk in two parts, for the class predictor (Walk with kTrack): begin()
+// makes round trip 2 (the window, start[q] and its start block, and q's
+// predictor entries) and the first step; finish() walks on to the class.
+// After begin(), `done` says whether the class is already known (in `cls`);
+// otherwise `slot` is the predictor entry that the way the first step left
+// the start block keys (-1: none) and `pc` the class recorded there (-1:
+// none).  The predictor entries of q are int32 [64 lanes][2 kinds].
+struct WalkRun {
+    Walk<false, true> w;
+    bool done;
+    int cls, slot, pc;
+
+    __device__ __forceinline__ void begin(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
+                                          int32_t n_classes, const int32_t *__restrict__ st, int len, int q,
+                                          int lane, const int32_t *__restrict__ pred) {
+        w = Walk<false, true>{table, st, n_lr, lane, len - 1, len - 1, 0, 0, -1, nullptr, 0};
+        done = false;
+        cls = -1;
+        slot = -1;
+        pc = -1;
+        const int nb = start_block_count(n_lex);
+        const int qb = min(q, nb - 1);
+        u32x4 bv = reinterpret_cast<const u32x4 *>(table - (int64_t)(nb - qb) * kStartBlockInts)[lane];
+        u32x2 pv = reinterpret_cast<const u32x2 *>(pred + (int64_t)qb * kPredInts)[lane];
+        w.sym = lane == kChunk ? table[q] : w.load(max(w.chunk_base - lane, 0));
+        asm volatile("" : "+v"(bv), "+v"(pv), "+v"(w.sym));
+        w.ref = __builtin_amdgcn_readlane(w.sym, kChunk);
+        if (w.ref < 0) {
+            done = true;
+            cls = -w.ref - 1;
+            return;
+        }
+        const bool has_block = q < nb;
+        if (!has_block) {
+            const int32_t *row = table + (w.ref & ~3);
+            if ((w.ref & 3) == kRefChain) bv = *reinterpret_cast<const u32x4 *>(row + kChainEntry * lane);
+            else if ((w.ref & 3) != kRefDense) bv.xy = *reinterpret_cast<const u32x2 *>(row + 2 * lane);
+        }
+        const bool dense = (w.ref & 3) == kRefDense;
+        if (w.first_step(make_int4((int)bv[0], (int)bv[1], (int)bv[2], (int)bv[3]))) {
+            done = true;
+            cls = w.cls;
+            return;
+        }
+        if (has_block && !dense) {
+            slot = (qb * kWave + w.exit_lane) * 2 + w.exit_kind;
+            const int p = __builtin_amdgcn_readlane((int)(w.exit_kind ? pv[1] : pv[0]), w.exit_lane);
+            pc = p >= 0 && p < n_classes ? p : -1;
+        }
+    }
+
+    __device__ __forceinline__ int finish() {
+        for (;;) {
+            w.ref = __builtin_amdgcn_readfirstlane(w.ref);
+            w.i = __builtin_amdgcn_readfirstlane(w.i);
+            w.chunk_base = __builtin_amdgcn_readfirstlane(w.chunk_base);
+            if (w.ref < 0) return w.ref == kRefFault ? -1 : -w.ref - 1;
+            if (w.i >= 0 && w.chunk_base - w.i >= kChunk) {
+                w.chunk_base = w.i;
+                w.stage();
+            }
+            if (w.step()) return w.cls;
+        }
+    }
+};
+
 // The lengths of sequences i0 + k * kWave + lane, k < kN, loaded in one
 // round trip (every load issued before the first is used), negative ones as
 // zero, summed per lane.
@@ -268,10 +350,11 @@ __device__ __forceinline__ int64_t lens_round(__amdgpu_buffer_rsrc_t rl, int i0,
 // (stride 0), the lengths before b (more round trips past 64 sequences):
 // the stack's offset, summed in 64 bits
 // (the stacks may hold more than 2^31 symbols in all), a negative length
-// counting as zero; with stride > 0 stack b starts at b * stride and holds at
-// most stride symbols.
+// counting as zero; a ragged stack reaching past n_stack symbols is an input
+// out of range, never read.  With stride > 0 stack b starts at b * stride
+// and holds at most stride symbols.
 __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
-                                          const int32_t *__restrict__ stacks, int32_t stride,
+                                          const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack,
                                           const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
                                           int b, int lane) {
     const int own = *((lane & 1) ? qs + b : lens + b);
@@ -289,7 +372,7 @@ __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int
     const int len = __builtin_amdgcn_readlane(own, 0);
     const int q = __builtin_amdgcn_readlane(own, 1);
     const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
-    if (len > 0 && (stride == 0 || len <= stride) && q >= 0 && q < n_lex)
+    if (len > 0 && (stride == 0 ? off + len <= n_stack : len <= stride) && q >= 0 && q < n_lex)
         return walk_class(table, n_lex, n_lr, stacks + off, len, q, lane);
     return -1;
 }
@@ -298,13 +381,13 @@ __device__ __forceinline__ int wave_class(const int32_t *__restrict__ table, int
 // published to the whole workgroup through LDS.  Slice 0 of each sequence
 // counts rejected inputs.
 __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
-                                           const int32_t *__restrict__ stacks, int32_t stride,
+                                           const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack,
                                            const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
                                            int b, uint32_t *__restrict__ err) {
     __shared__ int32_t s_cls;
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
-        const int cls = wave_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, lane);
+        const int cls = wave_class(table, n_lex, n_lr, stacks, stride, n_stack, lens, qs, b, lane);
         if (lane == 0) {
             s_cls = cls;
             if (cls < 0 && blockIdx.x == 0) atomicAdd(err, 1u);
@@ -314,35 +397,94 @@ __device__ __forceinline__ int block_class(const int32_t *__restrict__ table, in
     return s_cls;
 }
 
+// Round trip 1 and the start of the tracked walk of sequence b (the
+// predictor's form of wave_class): r.done with class -1 for an input out of
+// range.
+__device__ __forceinline__ void wave_begin(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr,
+                                           int32_t n_classes, const int32_t *__restrict__ stacks, int32_t stride,
+                                           int64_t n_stack, const int32_t *__restrict__ lens,
+                                           const int32_t *__restrict__ qs, const int32_t *__restrict__ pred, int b,
+                                           int lane, WalkRun &r) {
+    const int own = *((lane & 1) ? qs + b : lens + b);
+    int64_t part = 0;
+    if (stride == 0) {
+        const __amdgpu_buffer_rsrc_t rl = wave_rsrc(lens, (uint32_t)b * 4u);
+        if (b <= kWave) {
+            part = lens_round<1>(rl, 0, lane);
+        } else {
+            for (int i0 = 0; i0 < b; i0 += kLensPerRound * kWave) part += lens_round<kLensPerRound>(rl, i0, lane);
+        }
+    }
+    const int len = __builtin_amdgcn_readlane(own, 0);
+    const int q = __builtin_amdgcn_readlane(own, 1);
+    const int64_t off = stride ? (int64_t)b * stride : wave_sum(part);
+    if (len > 0 && (stride == 0 ? off + len <= n_stack : len <= stride) && q >= 0 && q < n_lex) {
+        r.begin(table, n_lex, n_lr, n_classes, stacks + off, len, q, lane, pred);
+    } else {
+        r.done = true;
+        r.cls = -1;
+        r.slot = -1;
+        r.pc = -1;
+    }
+}
+
+// After a tracked walk: record its class in the predictor entry its first
+// step keyed, when it differs from the prediction, and count the update.
+// Lane 0 of one wavefront per sequence.
+__device__ __forceinline__ void pred_update(int32_t *__restrict__ pred, uint32_t *__restrict__ counters,
+                                            const WalkRun &r, int cls) {
+    if (!r.done && r.slot >= 0 && cls >= 0 && cls != r.pc) {
+        pred[r.slot] = cls;
+        atomicAdd(counters + kCounterPredUpdates, 1u);
+    }
+}
+
 // psc_compute_classes: the walk alone (Algorithm 2, classification step),
-// one wavefront per sequence, kBlock / kWave sequences per workgroup.
+// one wavefront per sequence, kBlock / kWave sequences per workgroup.  It
+// fills the class predictor that the speculative step reads.
 __global__ void __launch_bounds__(kBlock)
-classes_kernel(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
-               int32_t stride, const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t B,
-               int32_t *__restrict__ out, uint32_t *__restrict__ err) {
+classes_kernel(const int32_t *__restrict__ table, int32_t n_lex, int32_t n_lr, int32_t n_classes,
+               const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack, const int32_t *__restrict__ lens,
+               const int32_t *__restrict__ qs, int32_t B, int32_t *__restrict__ out, uint32_t *__restrict__ counters,
+               int32_t *__restrict__ pred) {
     const int b = blockIdx.x * (kBlock / kWave) + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (b >= B) return;
     const int lane = threadIdx.x & (kWave - 1);
-    const int cls = wave_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, lane);
+    WalkRun r;
+    wave_begin(table, n_lex, n_lr, n_classes, stacks, stride, n_stack, lens, qs, pred, b, lane, r);
+    const int cls = r.done ? r.cls : r.finish();
     if (lane == 0) {
         out[b] = cls;
-        if (cls < 0) atomicAdd(err, 1u);
+        if (cls < 0) atomicAdd(counters + kCounterFaults, 1u);
+        pred_update(pred, counters, r, cls);
     }
+}
+
+// Word w of class c's mask row: rows[c * stride + w] in the flat layout;
+// with kSliced, rows[ids[c * stride + w / 64] * 64 + w % 64] (each distinct
+// 64-word slice of the rows stored once; stride = slices per row).
+template <bool kSliced>
+__device__ __forceinline__ const uint32_t *mask_at(const uint32_t *__restrict__ rows, int32_t stride,
+                                                   const int32_t *__restrict__ ids, int c, int w) {
+    if (kSliced)
+        return rows + (int64_t)ids[(int64_t)c * stride + (w >> 6)] * kSliceWords + (w & (kSliceWords - 1));
+    return rows + (int64_t)c * stride + w;
 }
 
 // One workgroup per (sequence b, slice of the mask row): the walk, then the
 // whole workgroup copies its slice of the class's precomputed mask row into
 // out_bitmask[b] (Algorithm 2, mask step).  Every slice of the same b repeats
 // the walk, which costs latency but no HBM bandwidth (the rows are cached).
+template <bool kSliced>
 __global__ void __launch_bounds__(kBlock)
 walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks,
-                   int32_t mask_stride, int32_t n_lex, int32_t n_lr,
-                   const int32_t *__restrict__ stacks, int32_t stride, const int32_t *__restrict__ lens,
-                   const int32_t *__restrict__ qs, int32_t B, int32_t W,
+                   int32_t mask_stride, const int32_t *__restrict__ ids, int32_t n_lex, int32_t n_lr,
+                   const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack,
+                   const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t B, int32_t W,
                    uint32_t *__restrict__ out, uint32_t *__restrict__ err, int32_t vec4) {
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, n_stack, lens, qs, b, err);
     const int w0 = blockIdx.x * kCopyWordsPerBlock;
     const int w1 = min(W, w0 + kCopyWordsPerBlock);
     uint32_t *dst = out + (size_t)b * W;
@@ -350,7 +492,7 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
         for (int w = w0 + tid; w < w1; w += kBlock) dst[w] = 0u;
         return;
     }
-    const uint32_t *src = masks + (size_t)cls * mask_stride;
+    const uint32_t *src = masks + (size_t)cls * mask_stride;   // the flat layout's row
     if (vec4) {
         // W % 4 == 0 and out is 16-byte aligned: 128-bit loads and stores
         // every load is issued before the first store, so no store waits
@@ -362,7 +504,9 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
 #pragma unroll
         for (int k = 0; k < kPer; k++) {
             const int w = w0 / 4 + tid + k * kBlock;
-            if (w < w1 / 4) v[k] = load_nt(s4 + w);
+            if (w < w1 / 4)
+                v[k] = kSliced ? load_nt(reinterpret_cast<const uint4 *>(mask_at<true>(masks, mask_stride, ids, cls, 4 * w)))
+                               : load_nt(s4 + w);
         }
 #pragma unroll
         for (int k = 0; k < kPer; k++) {
@@ -370,7 +514,7 @@ walk_gather_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict
             if (w < w1 / 4) store_nt(d4 + w, v[k]);
         }
     } else {
-        for (int w = w0 + tid; w < w1; w += kBlock) dst[w] = src[w];
+        for (int w = w0 + tid; w < w1; w += kBlock) dst[w] = *mask_at<kSliced>(masks, mask_stride, ids, cls, w);
     }
 }
 
@@ -494,10 +638,10 @@ constexpr int kFusedBlock = 4 * kWave;
 
 // The part of the fused step after the walk: this workgroup's slice of the
 // class's mask row, written to out_bitmask[b] and applied to logits[b].
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __device__ __forceinline__ void fused_fast_apply(int cls, int b, const uint32_t *__restrict__ masks,
-                                                 int32_t mask_stride, int32_t W, uint32_t *__restrict__ out,
-                                                 uint4 *__restrict__ logits) {
+                                                 int32_t mask_stride, const int32_t *__restrict__ ids, int32_t W,
+                                                 uint32_t *__restrict__ out, uint4 *__restrict__ logits) {
     using G = ApplyGeom<kBf16>;
     const int lane = threadIdx.x & (kWave - 1);
     const int w_base =
@@ -506,7 +650,7 @@ __device__ __forceinline__ void fused_fast_apply(int cls, int b, const uint32_t 
     uint32_t m = 0xFFFFFFFFu;
     const int w = w_base + lane;
     const bool mine = lane < G::kWordsPerWave && w < W;
-    if (mine) m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w];
+    if (mine) m = cls < 0 ? 0u : *mask_at<kSliced>(masks, mask_stride, ids, cls, w);
     const uint32_t words = (uint32_t)min(G::kWordsPerWave, W - w_base);
     apply_words<kBf16>(logits + ((size_t)b * W + w_base) * G::kVecsPerWord, words * G::kVecsPerWord * 16u, m,
                        lane);
@@ -514,15 +658,40 @@ __device__ __forceinline__ void fused_fast_apply(int cls, int b, const uint32_t 
     if (out && mine) out[(size_t)b * W + w] = m;
 }
 
-template <bool kBf16>
+// A timeline record per wavefront (psc_compute_and_apply_timeline): its
+// start, the prediction known (t_a), its class known (t_b) and its last
+// store issued, in ticks of the GPU's constant 100 MHz clock; then the
+// wavefront, its XCD, whether the prediction held and whether the class was
+// known at the first step; then the sequence and the slice.
+__device__ __forceinline__ void timeline_record(unsigned long long *__restrict__ tl, unsigned long long t0,
+                                                unsigned long long t_a, unsigned long long t_b, uint32_t held,
+                                                uint32_t early) {
+    const unsigned long long t_e = wall_clock64();
+    const uint32_t wave = threadIdx.x / kWave;
+    const uint32_t xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | (3 << 11)) & 15u;   // XCC_ID[3:0]
+    const size_t rec = ((size_t)blockIdx.y * gridDim.x + blockIdx.x) * (blockDim.x / kWave) + wave;
+    unsigned long long *o = tl + rec * 4;
+    o[0] = t0;
+    o[1] = (t_a - t0) | ((t_b - t0) << 32);
+    o[2] = (t_e - t0) | ((unsigned long long)(wave | (xcc << 3) | (held << 7) | (early << 8)) << 32);
+    o[3] = (unsigned long long)blockIdx.y | ((unsigned long long)blockIdx.x << 32);
+}
+
+// kTl: the timeline variant (profiling records, psc_compute_and_apply_timeline).
+template <bool kBf16, bool kSliced, bool kTl>
 __global__ void __launch_bounds__(kFusedBlock)
 fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                  int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
-                  const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
-                  uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
+                  const int32_t *__restrict__ ids, int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                  int32_t stride, int64_t n_stack, const int32_t *__restrict__ lens, const int32_t *__restrict__ qs,
+                  int32_t W, uint32_t *__restrict__ out, uint32_t *__restrict__ err, uint4 *__restrict__ logits,
+                  unsigned long long *__restrict__ tl) {
+    unsigned long long t0 = 0, t_b = 0;
+    if (kTl) t0 = wall_clock64();
     const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
-    fused_fast_apply<kBf16>(cls, b, masks, mask_stride, W, out, logits);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, n_stack, lens, qs, b, err);
+    if (kTl) t_b = wall_clock64();
+    fused_fast_apply<kBf16, kSliced>(cls, b, masks, mask_stride, ids, W, out, logits);
+    if (kTl && (threadIdx.x & (kWave - 1)) == 0) timeline_record(tl, t0, t0, t_b, 0u, 0u);
 }
 
 // psc_compute_and_apply, general path (any V, any element alignment): one
@@ -531,15 +700,16 @@ fused_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict_
 constexpr int kGenWords = 128;
 static_assert(kGenWords <= kBlock, "one pass stages the slice's words");
 
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __device__ __forceinline__ void fused_generic_apply(int cls, int b, const uint32_t *__restrict__ masks,
-                                                    int32_t mask_stride, int32_t V, int32_t W,
-                                                    uint32_t *__restrict__ out, void *__restrict__ logits) {
+                                                    int32_t mask_stride, const int32_t *__restrict__ ids, int32_t V,
+                                                    int32_t W, uint32_t *__restrict__ out,
+                                                    void *__restrict__ logits) {
     __shared__ uint32_t s_m[kGenWords];
     const int w0 = blockIdx.x * kGenWords;
     const int nw = min(kGenWords, W - w0);
     if (threadIdx.x < nw) {
-        const uint32_t m = cls < 0 ? 0u : masks[(size_t)cls * mask_stride + w0 + threadIdx.x];
+        const uint32_t m = cls < 0 ? 0u : *mask_at<kSliced>(masks, mask_stride, ids, cls, w0 + threadIdx.x);
         s_m[threadIdx.x] = m;
         if (out) out[(size_t)b * W + w0 + threadIdx.x] = m;
     }
@@ -553,15 +723,158 @@ __device__ __forceinline__ void fused_generic_apply(int cls, int b, const uint32
     }
 }
 
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __global__ void __launch_bounds__(kBlock)
 fused_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                     int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
-                     const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
-                     uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
+                     const int32_t *__restrict__ ids, int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks,
+                     int32_t stride, int64_t n_stack, const int32_t *__restrict__ lens,
+                     const int32_t *__restrict__ qs, int32_t V, int32_t W, uint32_t *__restrict__ out,
+                     uint32_t *__restrict__ err, void *__restrict__ logits) {
     const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
-    fused_generic_apply<kBf16>(cls, b, masks, mask_stride, V, W, out, logits);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, n_stack, lens, qs, b, err);
+    fused_generic_apply<kBf16, kSliced>(cls, b, masks, mask_stride, ids, V, W, out, logits);
+}
+
+// The speculative form of psc_compute_and_apply's fast path
+// (PSC_OPT_SPECULATE).  Wavefront 0 walks with the class predictor: after its
+// first step (two round trips in) it publishes the predicted class, or the
+// class itself when the walk has already ended (barrier A).  Wavefronts 1-3
+// then load their mask words of that class, and the logits vectors those
+// words leave partly allowed (the only ones whose old values the in-place
+// select needs), while the walk goes on; at barrier B, when the walk ends in
+// that class, they select and store at once, and otherwise load that
+// class's words and the partly allowed vectors they do not hold yet.
+// Wavefront 0 applies its own words after the walk, as in fused_fast_kernel.
+// Every result is that of fused_fast_kernel.
+struct SpecShared {
+    int32_t pc, done, cls;
+};
+
+template <bool kBf16>
+__device__ __forceinline__ void vector_groups(uint32_t m, int lane, uint32_t (&g)[ApplyGeom<kBf16>::kVecs]) {
+    using G = ApplyGeom<kBf16>;
+    constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
+#pragma unroll
+    for (int j = 0; j < G::kVecs; j++) {
+        const int v = j * kWave + lane;
+        g[j] = (__shfl(m, v / G::kVecsPerWord, kWave) >> ((v % G::kVecsPerWord) * G::kPerVec)) & kFull;
+    }
+}
+
+template <bool kBf16>
+__device__ __forceinline__ bool mixed_group(uint32_t g) {
+    constexpr uint32_t kFull = (1u << ApplyGeom<kBf16>::kPerVec) - 1;
+    return g != 0 && g != kFull;
+}
+
+template <bool kBf16, bool kSliced, bool kTl>
+__global__ void __launch_bounds__(kFusedBlock)
+fused_spec_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
+                  const int32_t *__restrict__ ids, int32_t n_lex, int32_t n_lr, int32_t n_classes,
+                  const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack,
+                  const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t W,
+                  uint32_t *__restrict__ out, uint32_t *__restrict__ counters, int32_t *__restrict__ pred,
+                  uint4 *__restrict__ logits, unsigned long long *__restrict__ tl) {
+    using G = ApplyGeom<kBf16>;
+    constexpr uint32_t kFull = (1u << G::kPerVec) - 1;
+    __shared__ SpecShared sh;
+    unsigned long long t0 = 0, t_a = 0, t_b = 0;
+    if (kTl) t0 = wall_clock64();
+    const int b = blockIdx.y;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int lane = threadIdx.x & (kWave - 1);
+    WalkRun r;
+    if (wave == 0) {
+        wave_begin(table, n_lex, n_lr, n_classes, stacks, stride, n_stack, lens, qs, pred, b, lane, r);
+        if (lane == 0) {
+            sh.done = r.done;
+            sh.pc = r.done ? r.cls : r.pc;
+        }
+    }
+    __syncthreads();                                             // A
+    if (kTl) t_a = wall_clock64();
+    const int done = sh.done, pc = sh.pc;
+    const int w_base = (blockIdx.x * (kFusedBlock / kWave) + wave) * G::kWordsPerWave;
+    const bool active = w_base < W;
+    const int w = w_base + lane;
+    const bool mine = active && lane < G::kWordsPerWave && w < W;
+    const uint32_t words = active ? (uint32_t)min(G::kWordsPerWave, W - w_base) : 0u;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        wave_rsrc(logits + ((size_t)b * W + (active ? w_base : 0)) * G::kVecsPerWord, words * G::kVecsPerWord * 16u);
+    const bool have = wave > 0 && (done || pc >= 0);
+    uint32_t mp = 0xFFFFFFFFu, gp[G::kVecs];
+    u32x4 xp[G::kVecs];
+#pragma unroll
+    for (int j = 0; j < G::kVecs; j++) {
+        gp[j] = kFull;
+        xp[j] = u32x4{0u, 0u, 0u, 0u};
+    }
+    int cls = -1;
+    if (wave == 0) {
+        cls = r.done ? r.cls : r.finish();
+        if (lane == 0) sh.cls = cls;
+    } else if (have && active) {
+        if (mine) mp = pc < 0 ? 0u : *mask_at<kSliced>(masks, mask_stride, ids, pc, w);
+        vector_groups<kBf16>(mp, lane, gp);
+#pragma unroll
+        for (int j = 0; j < G::kVecs; j++) {
+            const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
+            xp[j] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, mixed_group<kBf16>(gp[j]) ? off : kOffSkip, 0,
+                                                          kPolicyNt);
+        }
+    }
+    if (!done) __syncthreads();                                  // B
+    if (kTl) t_b = wall_clock64();
+    cls = done ? pc : sh.cls;
+    if (active) {
+        uint32_t m = mp, g[G::kVecs];
+        u32x4 x[G::kVecs];
+#pragma unroll
+        for (int j = 0; j < G::kVecs; j++) {
+            g[j] = gp[j];
+            x[j] = xp[j];
+        }
+        if (!(have && cls == pc)) {
+            m = 0xFFFFFFFFu;
+            if (mine) m = cls < 0 ? 0u : *mask_at<kSliced>(masks, mask_stride, ids, cls, w);
+            vector_groups<kBf16>(m, lane, g);
+            u32x4 y[G::kVecs];
+#pragma unroll
+            for (int j = 0; j < G::kVecs; j++) {
+                const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
+                const bool need = mixed_group<kBf16>(g[j]) && !mixed_group<kBf16>(gp[j]);
+                y[j] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, need ? off : kOffSkip, 0, kPolicyNt);
+            }
+#pragma unroll
+            for (int j = 0; j < G::kVecs; j++)
+                if (!mixed_group<kBf16>(gp[j])) x[j] = y[j];
+        }
+#pragma unroll
+        for (int j = 0; j < G::kVecs; j++) {
+            u32x4 val = x[j];
+            if (kBf16) {
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    const uint32_t lo = (g[j] >> (2 * k)) & 1 ? (val[k] & 0xFFFFu) : kBf16NegInf;
+                    const uint32_t hi = (g[j] >> (2 * k + 1)) & 1 ? (val[k] >> 16) : kBf16NegInf;
+                    val[k] = lo | (hi << 16);
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; k++)
+                    if (!((g[j] >> k) & 1)) val[k] = kF32NegInf;
+            }
+            const uint32_t off = (uint32_t)(j * kWave + lane) * 16u;
+            __builtin_amdgcn_raw_buffer_store_b128(val, rsrc, g[j] != kFull ? off : kOffSkip, 0, kPolicyStore);
+        }
+        // last, so that the logits accesses never wait for this store
+        if (out && mine) out[(size_t)b * W + w] = m;
+    }
+    if (wave == 0 && lane == 0 && blockIdx.x == 0) {
+        if (cls < 0) atomicAdd(counters + kCounterFaults, 1u);
+        pred_update(pred, counters, r, cls);
+    }
+    if (kTl && lane == 0) timeline_record(tl, t0, t_a, t_b, (uint32_t)(!done && cls == pc), (uint32_t)done);
 }
 
 // ---------------------------------------------------------------- masked argmax
@@ -598,21 +911,21 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long a, unsig
     return a > b ? a : b;
 }
 
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __global__ void __launch_bounds__(kFusedBlock)
 argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                      int32_t n_lex, int32_t n_lr, const int32_t *__restrict__ stacks, int32_t stride,
+                      const int32_t *__restrict__ ids, int32_t n_lex, int32_t n_lr,
+                      const int32_t *__restrict__ stacks, int32_t stride, int64_t n_stack,
                       const int32_t *__restrict__ lens, const int32_t *__restrict__ qs, int32_t V, int32_t W,
                       uint32_t *__restrict__ err, const void *__restrict__ logits, int32_t fast,
                       unsigned long long *__restrict__ records, int32_t *__restrict__ out_tokens) {
     using G = ApplyGeom<kBf16>;
     __shared__ unsigned long long s_best[kFusedBlock / kWave];
     const int b = blockIdx.y;
-    const int cls = block_class(table, n_lex, n_lr, stacks, stride, lens, qs, b, err);
+    const int cls = block_class(table, n_lex, n_lr, stacks, stride, n_stack, lens, qs, b, err);
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     unsigned long long best = 0;   // every real key is > 0
     if (cls >= 0) {
-        const uint32_t *mrow = masks + (size_t)cls * mask_stride;
         if (fast) {
             // the apply's layout: the wavefront's kWordsPerWave words, lane j
             // the vectors j, j + 64, ...; only vectors with an allowed token are read
@@ -620,7 +933,9 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
             const int w0 = (blockIdx.x * (kFusedBlock / kWave) + wave) * G::kWordsPerWave;
             if (w0 < W) {
                 const uint4 *row = reinterpret_cast<const uint4 *>(logits) + ((size_t)b * W + w0) * G::kVecsPerWord;
-                const uint32_t m = lane < G::kWordsPerWave && w0 + lane < W ? mrow[w0 + lane] : 0u;
+                const uint32_t m =
+                    lane < G::kWordsPerWave && w0 + lane < W ? *mask_at<kSliced>(masks, mask_stride, ids, cls, w0 + lane)
+                                                             : 0u;
                 uint32_t g[G::kVecs];
                 uint4 x[G::kVecs];
 #pragma unroll
@@ -647,7 +962,7 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
         } else {
             const int v_end = min(V, (blockIdx.x + 1) * kGenWords * 32);
             for (int v = blockIdx.x * kGenWords * 32 + threadIdx.x; v < v_end; v += kFusedBlock) {
-                if (!((mrow[v >> 5] >> (v & 31)) & 1u)) continue;
+                if (!((*mask_at<kSliced>(masks, mask_stride, ids, cls, v >> 5) >> (v & 31)) & 1u)) continue;
                 const size_t idx = (size_t)b * V + v;
                 const uint32_t f = kBf16 ? (uint32_t)reinterpret_cast<const uint16_t *>(logits)[idx] << 16
                                          : reinterpret_cast<const uint32_t *>(logits)[idx];
@@ -936,24 +1251,30 @@ advance_copy_kernel(DecodeArgs D) {
     }
 }
 
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __global__ void __launch_bounds__(kFusedBlock)
 decode_fast_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                   DecodeArgs D, int32_t W, uint32_t *__restrict__ out, uint32_t *__restrict__ err,
-                   uint4 *__restrict__ logits) {
+                   const int32_t *__restrict__ ids, DecodeArgs D, int32_t W, uint32_t *__restrict__ out,
+                   uint32_t *__restrict__ err, uint4 *__restrict__ logits) {
     const int b = blockIdx.y;
     const int cls = decode_block_class(table, D, b, err);
-    fused_fast_apply<kBf16>(cls, b, masks, mask_stride, W, out, logits);
+    fused_fast_apply<kBf16, kSliced>(cls, b, masks, mask_stride, ids, W, out, logits);
 }
 
-template <bool kBf16>
+template <bool kBf16, bool kSliced>
 __global__ void __launch_bounds__(kBlock)
 decode_generic_kernel(const int32_t *__restrict__ table, const uint32_t *__restrict__ masks, int32_t mask_stride,
-                      DecodeArgs D, int32_t V, int32_t W, uint32_t *__restrict__ out, uint32_t *__restrict__ err,
-                      void *__restrict__ logits) {
+                      const int32_t *__restrict__ ids, DecodeArgs D, int32_t V, int32_t W,
+                      uint32_t *__restrict__ out, uint32_t *__restrict__ err, void *__restrict__ logits) {
     const int b = blockIdx.y;
     const int cls = decode_block_class(table, D, b, err);
-    fused_generic_apply<kBf16>(cls, b, masks, mask_stride, V, W, out, logits);
+    fused_generic_apply<kBf16, kSliced>(cls, b, masks, mask_stride, ids, V, W, out, logits);
+}
+
+// Every predictor entry to the same value (psc_predictor_fill).
+__global__ void __launch_bounds__(kBlock)
+pred_fill_kernel(int32_t *__restrict__ pred, int64_t n, int32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) pred[i] = v;
 }
 
 psc_status device_fail(const char *what, hipError_t e) {
@@ -973,12 +1294,31 @@ psc_status check_bound(const psc_handle *h, const char *what) {
     return PSC_OK;
 }
 
-// The walk + gather kernel for ragged (stride 0) or strided stacks.
-psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
-                          const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *stream,
-                          const char *what) {
+// The bound tables as the kernels read them; mstride is the mask row
+// stride in words (flat) or the slices per row (sliced).
+struct Bound {
+    const int32_t *table;
+    const uint32_t *masks;
+    const int32_t *ids;
+    int32_t mstride;
+    uint32_t *err;
+    int32_t *pred;
+    bool sliced;
+};
+
+Bound bound(const psc_handle *h) {
+    char *base = static_cast<char *>(h->dev_base);
+    return Bound{reinterpret_cast<const int32_t *>(base + table_off(h->n_lex)),
+                 reinterpret_cast<const uint32_t *>(base + h->mask_off),
+                 reinterpret_cast<const int32_t *>(base + h->ids_off), h->sliced ? h->n_slices : h->mask_stride,
+                 reinterpret_cast<uint32_t *>(base), reinterpret_cast<int32_t *>(base + h->pred_off), h->sliced};
+}
+
+psc_status check_states(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
+                        const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, const void *out,
+                        const char *what) {
     if (psc_status st = check_bound(h, what)) return st;
-    if (B < 0 || stride < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_bitmask))) {
+    if (B < 0 || stride < 0 || n_stack < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out))) {
         set_error(std::string(what) + ": null argument or negative size");
         return PSC_E_INVALID_ARG;
     }
@@ -986,48 +1326,17 @@ psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t st
         set_error(std::string(what) + ": B > 65535");
         return PSC_E_INVALID_ARG;
     }
-    if (B == 0) return PSC_OK;
-    char *base = static_cast<char *>(h->dev_base);
-    const int32_t W = h->W;
-    const int vec4 = (W % 4 == 0) && ((reinterpret_cast<uintptr_t>(out_bitmask) & 15) == 0);
-    dim3 grid((W + kCopyWordsPerBlock - 1) / kCopyWordsPerBlock, B);
-    hipLaunchKernelGGL(walk_gather_kernel, grid, dim3(kBlock), 0, reinterpret_cast<hipStream_t>(stream),
-                       reinterpret_cast<const int32_t *>(base + table_off(h->n_lex)),
-                       reinterpret_cast<const uint32_t *>(base + h->mask_off), h->mask_stride, h->n_lex, h->n_lr,
-                       stacks, stride, stack_lens, lexer_states, B, W, out_bitmask,
-                       reinterpret_cast<uint32_t *>(base), vec4);
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+    return PSC_OK;
 }
 
-// The walk alone for ragged (stride 0) or strided stacks.
-psc_status launch_classes(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
-                          const int32_t *lexer_states, int32_t B, int32_t *out_classes, void *stream,
-                          const char *what) {
-    if (psc_status st = check_bound(h, what)) return st;
-    if (B < 0 || stride < 0 || (B > 0 && (!stacks || !stack_lens || !lexer_states || !out_classes))) {
-        set_error(std::string(what) + ": null argument or negative size");
+psc_status check_logits(const psc_handle *h, const void *logits, psc_dtype dtype, int32_t V, int32_t B,
+                        const char *what) {
+    if (dtype != PSC_F32 && dtype != PSC_BF16) {
+        set_error(std::string(what) + ": bad dtype");
         return PSC_E_INVALID_ARG;
     }
-    if (B == 0) return PSC_OK;
-    char *base = static_cast<char *>(h->dev_base);
-    const int per_block = kBlock / kWave;
-    hipLaunchKernelGGL(classes_kernel, dim3((B + per_block - 1) / per_block), dim3(kBlock), 0,
-                       reinterpret_cast<hipStream_t>(stream), reinterpret_cast<const int32_t *>(base + table_off(h->n_lex)),
-                       h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, B, out_classes,
-                       reinterpret_cast<uint32_t *>(base));
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? PSC_OK : device_fail(what, e);
-}
-
-// The single-launch step for ragged (stride 0) or strided stacks.
-psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
-                        const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask, void *logits,
-                        psc_dtype dtype, int32_t V, void *stream, const char *what) {
-    if (psc_status st = check_bound(h, what)) return st;
-    if (B < 0 || stride < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
-        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits))) {
-        set_error(std::string(what) + ": null argument, negative size or bad dtype");
+    if (B > 0 && !logits) {
+        set_error(std::string(what) + ": null logits");
         return PSC_E_INVALID_ARG;
     }
     if (V != h->V) {
@@ -1035,88 +1344,173 @@ psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stri
                   std::to_string(h->V) + ")");
         return PSC_E_INVALID_ARG;
     }
-    if (B > 65535) {
-        set_error(std::string(what) + ": B > 65535");
-        return PSC_E_INVALID_ARG;
-    }
-    if (B == 0) return PSC_OK;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
-    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
-    uint32_t *err = reinterpret_cast<uint32_t *>(base);
-    const int32_t W = h->W;
-    const bool bf16 = dtype == PSC_BF16;
-    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
-    if (fast) {
-        const int words_per_block = (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
-                                                                  : ApplyGeom<false>::kWordsPerWave);
-        dim3 grid((W + words_per_block - 1) / words_per_block, B);
-        if (bf16)
-            hipLaunchKernelGGL(fused_fast_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
-                               reinterpret_cast<uint4 *>(logits));
-        else
-            hipLaunchKernelGGL(fused_fast_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, W, out_bitmask, err,
-                               reinterpret_cast<uint4 *>(logits));
-    } else {
-        dim3 grid((W + kGenWords - 1) / kGenWords, B);
-        if (bf16)
-            hipLaunchKernelGGL(fused_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride,
-                               h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, out_bitmask,
-                               err, logits);
-        else
-            hipLaunchKernelGGL(fused_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
-                               h->mask_stride, h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W,
-                               out_bitmask, err, logits);
-    }
+    return PSC_OK;
+}
+
+psc_status launched(const char *what) {
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? PSC_OK : device_fail(what, e);
 }
 
-// The masked argmax for ragged (stride 0) or strided stacks.
-psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t stride, const int32_t *stack_lens,
-                         const int32_t *lexer_states, int32_t B, const void *logits, psc_dtype dtype, int32_t V,
-                         int32_t *out_tokens, void *stream, const char *what) {
-    if (psc_status st = check_bound(h, what)) return st;
-    if (B < 0 || stride < 0 || (dtype != PSC_F32 && dtype != PSC_BF16) ||
-        (B > 0 && (!stacks || !stack_lens || !lexer_states || !logits || !out_tokens))) {
-        set_error(std::string(what) + ": null argument, negative size or bad dtype");
-        return PSC_E_INVALID_ARG;
+// The walk + gather for ragged (stride 0) or strided stacks.
+psc_status launch_compute(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
+                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
+                          void *stream, const char *what) {
+    if (psc_status st = check_states(h, stacks, stride, n_stack, stack_lens, lexer_states, B, out_bitmask, what))
+        return st;
+    if (B == 0) return PSC_OK;
+    const Bound T = bound(h);
+    const int32_t W = h->W;
+    const int vec4 = (W % 4 == 0) && ((reinterpret_cast<uintptr_t>(out_bitmask) & 15) == 0);
+    dim3 grid((W + kCopyWordsPerBlock - 1) / kCopyWordsPerBlock, B);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (T.sliced)
+        hipLaunchKernelGGL(walk_gather_kernel<true>, grid, dim3(kBlock), 0, s, T.table, T.masks, T.mstride, T.ids,
+                           h->n_lex, h->n_lr, stacks, stride, n_stack, stack_lens, lexer_states, B, W, out_bitmask,
+                           T.err, vec4);
+    else
+        hipLaunchKernelGGL(walk_gather_kernel<false>, grid, dim3(kBlock), 0, s, T.table, T.masks, T.mstride, T.ids,
+                           h->n_lex, h->n_lr, stacks, stride, n_stack, stack_lens, lexer_states, B, W, out_bitmask,
+                           T.err, vec4);
+    return launched(what);
+}
+
+// The walk alone for ragged (stride 0) or strided stacks.
+psc_status launch_classes(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
+                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, int32_t *out_classes,
+                          void *stream, const char *what) {
+    if (psc_status st = check_states(h, stacks, stride, n_stack, stack_lens, lexer_states, B, out_classes, what))
+        return st;
+    if (B == 0) return PSC_OK;
+    const Bound T = bound(h);
+    const int per_block = kBlock / kWave;
+    hipLaunchKernelGGL(classes_kernel, dim3((B + per_block - 1) / per_block), dim3(kBlock), 0,
+                       reinterpret_cast<hipStream_t>(stream), T.table, h->n_lex, h->n_lr, h->n_classes, stacks,
+                       stride, n_stack, stack_lens, lexer_states, B, out_classes, T.err, T.pred);
+    return launched(what);
+}
+
+// Words of the mask row per fused workgroup on the fast path.
+int32_t fused_words_per_block(bool bf16) {
+    return (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave : ApplyGeom<false>::kWordsPerWave);
+}
+
+struct FastArgs {
+    dim3 grid;
+    hipStream_t s;
+    Bound T;
+    int32_t n_lex, n_lr, n_classes;
+    const int32_t *stacks;
+    int32_t stride;
+    int64_t n_stack;
+    const int32_t *lens, *qs;
+    int32_t W;
+    uint32_t *out;
+    uint4 *logits;
+    unsigned long long *tl;
+};
+
+template <bool kBf16, bool kSliced, bool kTl>
+void launch_fast(bool spec, const FastArgs &F) {
+    const Bound &T = F.T;
+    if (spec)
+        hipLaunchKernelGGL((fused_spec_kernel<kBf16, kSliced, kTl>), F.grid, dim3(kFusedBlock), 0, F.s, T.table,
+                           T.masks, T.mstride, T.ids, F.n_lex, F.n_lr, F.n_classes, F.stacks, F.stride, F.n_stack,
+                           F.lens, F.qs, F.W, F.out, T.err, T.pred, F.logits, F.tl);
+    else
+        hipLaunchKernelGGL((fused_fast_kernel<kBf16, kSliced, kTl>), F.grid, dim3(kFusedBlock), 0, F.s, T.table,
+                           T.masks, T.mstride, T.ids, F.n_lex, F.n_lr, F.stacks, F.stride, F.n_stack, F.lens, F.qs,
+                           F.W, F.out, T.err, F.logits, F.tl);
+}
+
+template <bool kBf16>
+void launch_fast_dtype(bool spec, bool sliced, bool tl, const FastArgs &F) {
+    if (sliced) {
+        if (tl) launch_fast<kBf16, true, true>(spec, F);
+        else launch_fast<kBf16, true, false>(spec, F);
+    } else {
+        if (tl) launch_fast<kBf16, false, true>(spec, F);
+        else launch_fast<kBf16, false, false>(spec, F);
     }
-    if (V != h->V) {
-        set_error(std::string(what) + ": V differs from the vocabulary size");
-        return PSC_E_INVALID_ARG;
-    }
-    if (B > 65535) {
-        set_error(std::string(what) + ": B > 65535");
-        return PSC_E_INVALID_ARG;
+}
+
+// The single-launch step for ragged (stride 0) or strided stacks; with
+// `tl` (fast path only) the timeline variant.
+psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
+                        const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
+                        void *logits, psc_dtype dtype, int32_t V, void *stream, const char *what,
+                        unsigned long long *tl = nullptr, int64_t n_tl = 0) {
+    // out_bitmask may be null: the logits stand in for it in the null check
+    if (psc_status st = check_states(h, stacks, stride, n_stack, stack_lens, lexer_states, B,
+                                     out_bitmask ? static_cast<const void *>(out_bitmask) : logits, what))
+        return st;
+    if (psc_status st = check_logits(h, logits, dtype, V, B, what)) return st;
+    const bool bf16 = dtype == PSC_BF16;
+    const bool fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+    const int32_t W = h->W;
+    if (tl) {
+        const int64_t need = (int64_t)((W + fused_words_per_block(bf16) - 1) / fused_words_per_block(bf16)) * B *
+                             (kFusedBlock / kWave);
+        if (!fast || n_tl < need) {
+            set_error(std::string(what) + ": the timeline needs the fast path (V % 32 == 0, 16-byte aligned "
+                      "logits) and " + std::to_string(need) + " records");
+            return PSC_E_INVALID_ARG;
+        }
     }
     if (B == 0) return PSC_OK;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const Bound T = bound(h);
+    if (fast) {
+        const FastArgs F{dim3((W + fused_words_per_block(bf16) - 1) / fused_words_per_block(bf16), B), s, T,
+                         h->n_lex, h->n_lr, h->n_classes, stacks, stride, n_stack, stack_lens, lexer_states, W,
+                         out_bitmask, reinterpret_cast<uint4 *>(logits), tl};
+        const bool spec = (h->options & PSC_OPT_SPECULATE) != 0;
+        if (bf16) launch_fast_dtype<true>(spec, T.sliced, tl != nullptr, F);
+        else launch_fast_dtype<false>(spec, T.sliced, tl != nullptr, F);
+    } else {
+        dim3 grid((W + kGenWords - 1) / kGenWords, B);
+#define PSC_GENERIC(BF, SL)                                                                                          \
+    hipLaunchKernelGGL((fused_generic_kernel<BF, SL>), grid, dim3(kBlock), 0, s, T.table, T.masks, T.mstride, T.ids,  \
+                       h->n_lex, h->n_lr, stacks, stride, n_stack, stack_lens, lexer_states, V, W, out_bitmask,     \
+                       T.err, logits)
+        if (bf16 && T.sliced) PSC_GENERIC(true, true);
+        else if (bf16) PSC_GENERIC(true, false);
+        else if (T.sliced) PSC_GENERIC(false, true);
+        else PSC_GENERIC(false, false);
+#undef PSC_GENERIC
+    }
+    return launched(what);
+}
+
+// The masked argmax for ragged (stride 0) or strided stacks.
+psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
+                         const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, const void *logits,
+                         psc_dtype dtype, int32_t V, int32_t *out_tokens, void *stream, const char *what) {
+    if (psc_status st = check_states(h, stacks, stride, n_stack, stack_lens, lexer_states, B, out_tokens, what))
+        return st;
+    if (psc_status st = check_logits(h, logits, dtype, V, B, what)) return st;
+    if (B == 0) return PSC_OK;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
-    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
-    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const Bound T = bound(h);
     const int fast = (V % 32 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
     const int32_t W = h->W;
-    const int words_per_block = !fast ? kGenWords
-                                      : (kFusedBlock / kWave) * (dtype == PSC_BF16 ? ApplyGeom<true>::kWordsPerWave
-                                                                                   : ApplyGeom<false>::kWordsPerWave);
+    const int words_per_block = !fast ? kGenWords : fused_words_per_block(dtype == PSC_BF16);
     dim3 grid((W + words_per_block - 1) / words_per_block, B);
     auto *records = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
-    if (dtype == PSC_BF16)
-        hipLaunchKernelGGL(argmax_partial_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
-                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
-                           records, out_tokens);
-    else
-        hipLaunchKernelGGL(argmax_partial_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
-                           h->n_lex, h->n_lr, stacks, stride, stack_lens, lexer_states, V, W, err, logits, fast,
-                           records, out_tokens);
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? PSC_OK : device_fail(what, e);
+#define PSC_ARGMAX(BF, SL)                                                                                           \
+    hipLaunchKernelGGL((argmax_partial_kernel<BF, SL>), grid, dim3(kFusedBlock), 0, s, T.table, T.masks, T.mstride,   \
+                       T.ids, h->n_lex, h->n_lr, stacks, stride, n_stack, stack_lens, lexer_states, V, W, T.err,    \
+                       logits, fast, records, out_tokens)
+    if (dtype == PSC_BF16 && T.sliced) PSC_ARGMAX(true, true);
+    else if (dtype == PSC_BF16) PSC_ARGMAX(true, false);
+    else if (T.sliced) PSC_ARGMAX(false, true);
+    else PSC_ARGMAX(false, false);
+#undef PSC_ARGMAX
+    return launched(what);
 }
+
+constexpr int64_t kUnbounded = INT64_MAX;
 
 psc_status check_dense(const int32_t *stacks, int32_t cap, const int32_t *lens, const int32_t *qs, int32_t B,
                        const char *what) {
@@ -1161,26 +1555,24 @@ bool ranges_overlap(const void *a, const void *b, size_t n) {
 
 }  // namespace
 
-extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream) {
+extern "C" psc_status psc_bind_device_ex(psc_handle *h, void *dev_buf, size_t nbytes, uint32_t flags,
+                                         void *stream) {
     if (!h || !dev_buf || (reinterpret_cast<uintptr_t>(dev_buf) & 255) != 0) {
         set_error("psc_bind_device: null handle/buffer or buffer not 256-byte aligned");
         return PSC_E_INVALID_ARG;
     }
-    size_t need = h->device_bytes_needed();
-    if (nbytes < need) {
-        set_error("psc_bind_device: buffer too small (" + std::to_string(nbytes) + " < " + std::to_string(need) + ")");
+    if (flags & ~(uint32_t)(PSC_BIND_FLAT | PSC_BIND_SLICED) || flags == (PSC_BIND_FLAT | PSC_BIND_SLICED)) {
+        set_error("psc_bind_device: unknown flags");
         return PSC_E_INVALID_ARG;
     }
-    auto up = [](size_t n) { return (n + 255) & ~(size_t)255; };
+    const DeviceLayout L = device_layout(*h, flags);
+    if (nbytes < L.total) {
+        set_error("psc_bind_device: buffer too small (" + std::to_string(nbytes) + " < " + std::to_string(L.total) +
+                  ")");
+        return PSC_E_INVALID_ARG;
+    }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(dev_buf);
-    const size_t tab_off = table_off(h->n_lex);
-    const size_t mask_off = tab_off + up(h->table.size() * sizeof(int32_t));
-    const size_t gram_off = mask_off + up(h->masks.size() * sizeof(uint32_t));
-    const size_t vbytes_off = gram_off + up(h->gram.size() * sizeof(int32_t));
-    const size_t argmax_off = vbytes_off + up(h->vbytes.size());
-    const size_t packed_off = argmax_off + kArgmaxBytes;
-    const size_t closure_off = packed_off + up((size_t)h->n_lr * h->adv.n_term * sizeof(int32_t));
     // the tables derived at bind time, on the host first
     std::vector<int32_t> packed, closure, blocks;
     bool is_packed = false;
@@ -1193,52 +1585,74 @@ extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbyte
         return PSC_E_OOM;
     }
     hipError_t e = hipMemsetAsync(base, 0, kStartBlockOff, s);
+    auto put = [&](size_t off, const void *src, size_t n) {
+        if (e == hipSuccess && n) e = hipMemcpyAsync(base + off, src, n, hipMemcpyHostToDevice, s);
+    };
+    put(kStartBlockOff, blocks.data(), blocks.size() * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemsetAsync(base + L.argmax, 0, kArgmaxBytes, s);
+    put(L.table, h->table.data(), h->table.size() * sizeof(int32_t));
+    if (L.sliced) {
+        put(L.masks, h->slices.data(), h->slices.size() * sizeof(uint32_t));
+        put(L.ids, h->slice_ids.data(), h->slice_ids.size() * sizeof(int32_t));
+    } else {
+        put(L.masks, h->masks.data(), h->masks.size() * sizeof(uint32_t));
+    }
+    put(L.gram, h->gram.data(), h->gram.size() * sizeof(int32_t));
+    put(L.vbytes, h->vbytes.data(), h->vbytes.size());
+    if (is_packed) put(L.packed, packed.data(), packed.size() * sizeof(int32_t));
+    if (!closure.empty()) put(L.closure, closure.data(), closure.size() * sizeof(int32_t));
+    // the predictor starts empty (-1 in every entry)
     if (e == hipSuccess)
-        e = hipMemcpyAsync(base + kStartBlockOff, blocks.data(), blocks.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipMemsetAsync(base + argmax_off, 0, kArgmaxBytes, s);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(base + tab_off, h->table.data(), h->table.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, s);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(base + mask_off, h->masks.data(), h->masks.size() * sizeof(uint32_t),
-                           hipMemcpyHostToDevice, s);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(base + gram_off, h->gram.data(), h->gram.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, s);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(base + vbytes_off, h->vbytes.data(), h->vbytes.size(), hipMemcpyHostToDevice, s);
-    if (e == hipSuccess && is_packed)
-        e = hipMemcpyAsync(base + packed_off, packed.data(), packed.size() * sizeof(int32_t), hipMemcpyHostToDevice,
-                           s);
-    if (e == hipSuccess && !closure.empty())
-        e = hipMemcpyAsync(base + closure_off, closure.data(), closure.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, s);
+        e = hipMemsetAsync(base + L.pred, 0xFF, (size_t)start_block_count(h->n_lex) * kPredInts * sizeof(int32_t), s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return device_fail("psc_bind_device", e);
     h->dev_base = dev_buf;
     h->dev_bytes = nbytes;
-    h->mask_off = mask_off;
-    h->gram_off = gram_off;
-    h->vbytes_off = vbytes_off;
-    h->argmax_off = argmax_off;
-    h->packed_off = packed_off;
+    h->sliced = L.sliced;
+    h->mask_off = L.masks;
+    h->ids_off = L.ids;
+    h->gram_off = L.gram;
+    h->vbytes_off = L.vbytes;
+    h->argmax_off = L.argmax;
+    h->packed_off = L.packed;
     h->action_packed = is_packed;
-    h->closure_off = closure_off;
+    h->closure_off = L.closure;
     h->has_closure = !closure.empty();
+    h->pred_off = L.pred;
+    h->info.bound_mask_layout = L.sliced ? PSC_BIND_SLICED : PSC_BIND_FLAT;
     return PSC_OK;
+}
+
+extern "C" psc_status psc_bind_device(psc_handle *h, void *dev_buf, size_t nbytes, void *stream) {
+    return psc_bind_device_ex(h, dev_buf, nbytes, 0, stream);
 }
 
 extern "C" psc_status psc_compute_masks(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                         const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
                                         void *stream) {
-    return launch_compute(h, stacks, 0, stack_lens, lexer_states, B, out_bitmask, stream, "psc_compute_masks");
+    return launch_compute(h, stacks, 0, kUnbounded, stack_lens, lexer_states, B, out_bitmask, stream,
+                          "psc_compute_masks");
+}
+
+extern "C" psc_status psc_compute_masks_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                          uint32_t *out_bitmask, void *stream) {
+    return launch_compute(h, stacks, 0, n_stack, stack_lens, lexer_states, B, out_bitmask, stream,
+                          "psc_compute_masks_n");
 }
 
 extern "C" psc_status psc_compute_classes(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                           const int32_t *lexer_states, int32_t B, int32_t *out_classes,
                                           void *stream) {
-    return launch_classes(h, stacks, 0, stack_lens, lexer_states, B, out_classes, stream, "psc_compute_classes");
+    return launch_classes(h, stacks, 0, kUnbounded, stack_lens, lexer_states, B, out_classes, stream,
+                          "psc_compute_classes");
+}
+
+extern "C" psc_status psc_compute_classes_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                            const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                            int32_t *out_classes, void *stream) {
+    return launch_classes(h, stacks, 0, n_stack, stack_lens, lexer_states, B, out_classes, stream,
+                          "psc_compute_classes_n");
 }
 
 extern "C" psc_status psc_compute_classes_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
@@ -1246,22 +1660,49 @@ extern "C" psc_status psc_compute_classes_dense(const psc_handle *h, const int32
                                                 int32_t *out_classes, void *stream) {
     if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_classes_dense"))
         return st;
-    return launch_classes(h, stacks, cap, stack_lens, lexer_states, B, out_classes, stream,
+    return launch_classes(h, stacks, cap, kUnbounded, stack_lens, lexer_states, B, out_classes, stream,
                           "psc_compute_classes_dense");
 }
 
 extern "C" psc_status psc_compute_and_apply(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                             const int32_t *lexer_states, int32_t B, uint32_t *out_bitmask,
                                             void *logits, psc_dtype dtype, int32_t V, void *stream) {
-    return launch_fused(h, stacks, 0, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
+    return launch_fused(h, stacks, 0, kUnbounded, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
                         "psc_compute_and_apply");
+}
+
+extern "C" psc_status psc_compute_and_apply_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                              const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                              uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V,
+                                              void *stream) {
+    return launch_fused(h, stacks, 0, n_stack, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
+                        "psc_compute_and_apply_n");
+}
+
+extern "C" int64_t psc_timeline_records(const psc_handle *h, int32_t B, psc_dtype dtype) {
+    if (!h || B < 0) return 0;
+    const int32_t per = fused_words_per_block(dtype == PSC_BF16);
+    return (int64_t)((h->W + per - 1) / per) * B * (kFusedBlock / kWave);
+}
+
+extern "C" psc_status psc_compute_and_apply_timeline(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                                     const int32_t *stack_lens, const int32_t *lexer_states,
+                                                     int32_t B, uint32_t *out_bitmask, void *logits,
+                                                     psc_dtype dtype, int32_t V, uint64_t *records,
+                                                     int64_t n_records, void *stream) {
+    if (!records) {
+        set_error("psc_compute_and_apply_timeline: null records");
+        return PSC_E_INVALID_ARG;
+    }
+    return launch_fused(h, stacks, 0, n_stack, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
+                        "psc_compute_and_apply_timeline", reinterpret_cast<unsigned long long *>(records), n_records);
 }
 
 extern "C" psc_status psc_compute_masks_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
                                               const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
                                               uint32_t *out_bitmask, void *stream) {
     if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_masks_dense")) return st;
-    return launch_compute(h, stacks, cap, stack_lens, lexer_states, B, out_bitmask, stream,
+    return launch_compute(h, stacks, cap, kUnbounded, stack_lens, lexer_states, B, out_bitmask, stream,
                           "psc_compute_masks_dense");
 }
 
@@ -1271,15 +1712,23 @@ extern "C" psc_status psc_compute_and_apply_dense(const psc_handle *h, const int
                                                   void *stream) {
     if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_and_apply_dense"))
         return st;
-    return launch_fused(h, stacks, cap, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V, stream,
-                        "psc_compute_and_apply_dense");
+    return launch_fused(h, stacks, cap, kUnbounded, stack_lens, lexer_states, B, out_bitmask, logits, dtype, V,
+                        stream, "psc_compute_and_apply_dense");
 }
 
 extern "C" psc_status psc_compute_and_argmax(const psc_handle *h, const int32_t *stacks, const int32_t *stack_lens,
                                              const int32_t *lexer_states, int32_t B, const void *logits,
                                              psc_dtype dtype, int32_t V, int32_t *out_tokens, void *stream) {
-    return launch_argmax(h, stacks, 0, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
+    return launch_argmax(h, stacks, 0, kUnbounded, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
                          "psc_compute_and_argmax");
+}
+
+extern "C" psc_status psc_compute_and_argmax_n(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                               const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                               const void *logits, psc_dtype dtype, int32_t V, int32_t *out_tokens,
+                                               void *stream) {
+    return launch_argmax(h, stacks, 0, n_stack, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
+                         "psc_compute_and_argmax_n");
 }
 
 extern "C" psc_status psc_compute_and_argmax_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
@@ -1288,8 +1737,44 @@ extern "C" psc_status psc_compute_and_argmax_dense(const psc_handle *h, const in
                                                    int32_t *out_tokens, void *stream) {
     if (psc_status st = check_dense(stacks, cap, stack_lens, lexer_states, B, "psc_compute_and_argmax_dense"))
         return st;
-    return launch_argmax(h, stacks, cap, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
-                         "psc_compute_and_argmax_dense");
+    return launch_argmax(h, stacks, cap, kUnbounded, stack_lens, lexer_states, B, logits, dtype, V, out_tokens,
+                         stream, "psc_compute_and_argmax_dense");
+}
+
+extern "C" psc_status psc_set_options(psc_handle *h, uint32_t options) {
+    if (!h || (options & ~(uint32_t)PSC_OPT_SPECULATE)) {
+        set_error("psc_set_options: null handle or unknown option");
+        return PSC_E_INVALID_ARG;
+    }
+    h->options = options;
+    return PSC_OK;
+}
+
+extern "C" psc_status psc_predictor_fill(const psc_handle *h, int32_t cls, void *stream) {
+    if (psc_status st = check_bound(h, "psc_predictor_fill")) return st;
+    if (cls < -1 || cls >= h->n_classes) {
+        set_error("psc_predictor_fill: class out of range");
+        return PSC_E_INVALID_ARG;
+    }
+    const int64_t n = (int64_t)start_block_count(h->n_lex) * kPredInts;
+    hipLaunchKernelGGL(pred_fill_kernel, dim3((unsigned)std::min<int64_t>((n + kBlock - 1) / kBlock, 4096)),
+                       dim3(kBlock), 0, reinterpret_cast<hipStream_t>(stream),
+                       reinterpret_cast<int32_t *>(static_cast<char *>(h->dev_base) + h->pred_off), n, cls);
+    return launched("psc_predictor_fill");
+}
+
+extern "C" psc_status psc_predictor_updates(const psc_handle *h, uint32_t *out, int32_t reset, void *stream) {
+    if (!out) {
+        set_error("psc_predictor_updates: null argument");
+        return PSC_E_INVALID_ARG;
+    }
+    if (psc_status st = check_bound(h, "psc_predictor_updates")) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    uint32_t *ctr = static_cast<uint32_t *>(h->dev_base) + kCounterPredUpdates;
+    hipError_t e = hipMemcpyAsync(out, ctr, sizeof(uint32_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess && reset) e = hipMemsetAsync(ctr, 0, sizeof(uint32_t), s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    return e == hipSuccess ? PSC_OK : device_fail("psc_predictor_updates", e);
 }
 
 extern "C" psc_status psc_state_reset(const psc_handle *h, int32_t *stacks, int32_t cap, int32_t *stack_lens,
@@ -1354,9 +1839,7 @@ extern "C" psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks
     }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     char *base = static_cast<char *>(h->dev_base);
-    const int32_t *table = reinterpret_cast<const int32_t *>(base + table_off(h->n_lex));
-    const uint32_t *masks = reinterpret_cast<const uint32_t *>(base + h->mask_off);
-    uint32_t *err = reinterpret_cast<uint32_t *>(base);
+    const Bound T = bound(h);
     const DecodeArgs D{adv_tables(h), stacks_in, lens_in, qs_in, stacks_out, lens_out, qs_out, tokens, status, cap};
     const int32_t W = h->W;
     const bool bf16 = dtype == PSC_BF16;
@@ -1373,26 +1856,31 @@ extern "C" psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks
         hipLaunchKernelGGL(advance_copy_kernel, dim3(B), dim3(kWave), 0, s, D);
         hipError_t e0 = hipGetLastError();
         if (e0 != hipSuccess) return device_fail(what, e0);
-        return launch_fused(h, stacks_out, cap, lens_out, qs_out, B, out_bitmask, logits, dtype, V, stream, what);
+        return launch_fused(h, stacks_out, cap, kUnbounded, lens_out, qs_out, B, out_bitmask, logits, dtype, V, stream,
+                            what);
     }
     if (fast) {
         const int words_per_block = (kFusedBlock / kWave) * (bf16 ? ApplyGeom<true>::kWordsPerWave
                                                                   : ApplyGeom<false>::kWordsPerWave);
         dim3 grid((W + words_per_block - 1) / words_per_block, B);
-        if (bf16)
-            hipLaunchKernelGGL(decode_fast_kernel<true>, grid, dim3(kFusedBlock), 0, s, table, masks, h->mask_stride,
-                               D, W, out_bitmask, err, reinterpret_cast<uint4 *>(logits));
-        else
-            hipLaunchKernelGGL(decode_fast_kernel<false>, grid, dim3(kFusedBlock), 0, s, table, masks,
-                               h->mask_stride, D, W, out_bitmask, err, reinterpret_cast<uint4 *>(logits));
+#define PSC_DECODE_FAST(BF, SL)                                                                                      \
+    hipLaunchKernelGGL((decode_fast_kernel<BF, SL>), grid, dim3(kFusedBlock), 0, s, T.table, T.masks, T.mstride, T.ids, \
+                       D, W, out_bitmask, T.err, reinterpret_cast<uint4 *>(logits))
+        if (bf16 && T.sliced) PSC_DECODE_FAST(true, true);
+        else if (bf16) PSC_DECODE_FAST(true, false);
+        else if (T.sliced) PSC_DECODE_FAST(false, true);
+        else PSC_DECODE_FAST(false, false);
+#undef PSC_DECODE_FAST
     } else {
         dim3 grid((W + kGenWords - 1) / kGenWords, B);
-        if (bf16)
-            hipLaunchKernelGGL(decode_generic_kernel<true>, grid, dim3(kBlock), 0, s, table, masks, h->mask_stride, D,
-                               V, W, out_bitmask, err, logits);
-        else
-            hipLaunchKernelGGL(decode_generic_kernel<false>, grid, dim3(kBlock), 0, s, table, masks,
-                               h->mask_stride, D, V, W, out_bitmask, err, logits);
+#define PSC_DECODE_GEN(BF, SL)                                                                                       \
+    hipLaunchKernelGGL((decode_generic_kernel<BF, SL>), grid, dim3(kBlock), 0, s, T.table, T.masks, T.mstride, T.ids,   \
+                       D, V, W, out_bitmask, T.err, logits)
+        if (bf16 && T.sliced) PSC_DECODE_GEN(true, true);
+        else if (bf16) PSC_DECODE_GEN(true, false);
+        else if (T.sliced) PSC_DECODE_GEN(false, true);
+        else PSC_DECODE_GEN(false, false);
+#undef PSC_DECODE_GEN
     }
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? PSC_OK : device_fail(what, e);

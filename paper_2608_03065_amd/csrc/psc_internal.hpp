@@ -69,21 +69,33 @@ struct AdvanceLayout {
     int32_t n_term = 0, n_nt = 0, end_term = 0, eos = -1;
 };
 
-// Device buffer layout (offsets in bytes from the bound base):
-//   [0, 256)                   uint32 error counter (+ padding)
+// Device buffer layout (offsets in bytes from the bound base; device_layout
+// computes them):
+//   [0, 256)                   uint32 counters: [0] inputs rejected by a walk (range
+//                              faults), [1] updates of the class predictor (+ padding)
 //   [256, table_off(n_lex))    start blocks [min(n_lex, kMaxStartBlocks)][64 lanes][4] int32: block q holds the
 //                              first walk step's wavefront load from start[q] (the 64
 //                              chain entries, or the sparse row's pairs in .x/.y), so that
 //                              it is fetched together with the stack instead of after it
 //   [table_off(n_lex), ...)    int32 table: start refs [n_lex], rows, pad
-//   [mask_off, ...)            uint32 masks [n_classes][mask_stride] (256-B aligned)
+//   [mask_off, ...)            flat layout: uint32 masks [n_classes][mask_stride] (256-B aligned);
+//                              sliced layout: uint32 slices [n_unique_slices][64], then
+//                              int32 slice ids [n_classes][n_slices] at ids_off (row c of
+//                              the flat table is slices[ids[c][0]], slices[ids[c][1]], ...)
 //   [gram_off, ...)            int32 advance blob (AdvanceLayout)
 //   [vbytes_off, ...)          uint8 vocabulary bytes
 //   [argmax_off, ...)          masked argmax: [65536] records of 128 bytes, each a uint64
 //                              slot then a uint32 arrival counter (zero between calls)
 //   [packed_off, ...)          int32 ACTION with packed reductions (packed_action)
 //   [closure_off, ...)         int32 unit-reduction closure of GOTO (goto_closure), when it fits
+//   [pred_off, ...)            int32 class predictor [start_block_count(n_lex)][64][2]: for
+//                              lexer state q and the way a walk's first step from start[q]
+//                              left the start block (lane, kind), the class such a walk last
+//                              reached; -1 = none
 constexpr size_t kStartBlockOff = 256;
+constexpr int kCounterFaults = 0, kCounterPredUpdates = 1;
+constexpr int kSliceWords = 64;           // words per slice of a mask row (the sliced layout)
+constexpr int kPredInts = 64 * 2;         // predictor slots per lexer state
 constexpr int kStartBlockInts = 64 * 4;   // one 16-byte vector per lane
 // Lexer states q < kMaxStartBlocks have a start block (at most 4 MB); a walk
 // from a higher one reads start[q]'s row after start[q], as any other row.
@@ -107,13 +119,21 @@ struct psc_handle {
     std::vector<uint8_t> vbytes;   // vocabulary bytes (at least 1)
     psc::AdvanceLayout adv;
     psc_info_t info{};
+    // the mask table cut into kSliceWords-word slices, each distinct slice
+    // stored once (slice_masks): n_slices = mask_stride / kSliceWords per row
+    std::vector<uint32_t> slices;  // [n_unique_slices][kSliceWords]
+    std::vector<int32_t> slice_ids;   // [n_classes][n_slices]
+    int32_t n_slices = 0, n_unique_slices = 0;
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
-    size_t mask_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0, closure_off = 0;
+    size_t mask_off = 0, ids_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0,
+           closure_off = 0, pred_off = 0;
+    bool sliced = false;           // the bound mask table is the sliced layout
+    uint32_t options = 0;          // PSC_OPT_* (psc_set_options)
     bool action_packed = false;    // the device ACTION copy carries each reduction's length and lhs
     bool has_closure = false;      // the device holds the unit-reduction closure of GOTO
-    size_t device_bytes_needed() const;
+    size_t device_bytes_needed(uint32_t flags = 0) const;
 };
 
 namespace psc {
@@ -141,4 +161,14 @@ void goto_closure(const psc_handle &h, std::vector<int32_t> &out);
 void start_blocks(const psc_handle &h, std::vector<int32_t> &out);
 // The input checks of psc_build (ids in range, spellings), for loaded tables.
 psc_status check_instance(const psc_grammar *g, const psc_vocab *v, std::string *msg);
+// Cut the mask table into kSliceWords-word slices and keep each distinct
+// slice once (h.slices, h.slice_ids); fills the sliced-layout fields of h.info.
+void slice_masks(psc_handle &h);
+// Byte offsets of every region of the bound buffer for the mask layout that
+// `flags` selects (PSC_BIND_FLAT or PSC_BIND_SLICED; 0 = the default).
+struct DeviceLayout {
+    bool sliced;
+    size_t table, masks, ids, gram, vbytes, argmax, packed, closure, pred, total;
+};
+DeviceLayout device_layout(const psc_handle &h, uint32_t flags);
 }

@@ -329,6 +329,7 @@ extern "C" psc_status psc_load(const char *path, psc_handle **out) {
         h->info.n_classes = h->n_classes;
         h->info.table_bytes = (int64_t)h->table.size() * 4;
         h->info.mask_table_bytes = (int64_t)h->masks.size() * 4;
+        slice_masks(*h);
         h->info.device_bytes = (int64_t)h->device_bytes_needed();
         *out = h.release();
         return PSC_OK;

@@ -25,7 +25,14 @@ EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc
             "psc_compute_masks_dense", "psc_compute_and_apply_dense", "psc_compute_and_argmax",
             "psc_compute_and_argmax_dense", "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step",
             "psc_save", "psc_load", "psc_device_error_count", "psc_classify_host", "psc_class_mask_host",
-            "psc_host_state", "psc_free", "psc_last_error"]
+            "psc_host_state", "psc_free", "psc_last_error", "psc_device_bytes_ex", "psc_bind_device_ex",
+            "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n", "psc_compute_and_argmax_n",
+            "psc_predictor_fill", "psc_predictor_updates", "psc_timeline_records", "psc_compute_and_apply_timeline",
+            "psc_set_options"]
+
+BIND_FLAT, BIND_SLICED = 1, 2
+OPT_SPECULATE = 1
+_LAYOUTS = {None: 0, "default": 0, "flat": BIND_FLAT, "sliced": BIND_SLICED}
 
 
 class PscError(RuntimeError):
@@ -37,7 +44,8 @@ class PscError(RuntimeError):
 # Argument checks (not asserts, so that python -O keeps them): the library
 # trusts the sizes it is given, so a tensor of the wrong shape, dtype or
 # device must never reach it.  (The lengths of ragged stacks live on the
-# device and are not checked here: `stacks` must hold their sum.)
+# device: the calls pass stacks.numel() to the *_n entry points, which
+# reject a sequence whose stack would reach past it.)
 def _require(ok: bool, what: str) -> None:
     if not ok:
         raise ValueError(f"psc: expected {what}")
@@ -137,7 +145,8 @@ class Info(C.Structure):
         ("dfa_states_built", C.c_int64), ("dfa_states", C.c_int32), ("dfa_rows", C.c_int32),
         ("dense_rows", C.c_int32), ("max_sparse_edges", C.c_int32), ("table_bytes", C.c_int64),
         ("mask_table_bytes", C.c_int64), ("device_bytes", C.c_int64), ("build_seconds", C.c_double),
-        ("chain_states", C.c_int32), ("chains", C.c_int32),
+        ("chain_states", C.c_int32), ("chains", C.c_int32), ("mask_slices_unique", C.c_int32),
+        ("bound_mask_layout", C.c_int32), ("sliced_mask_bytes", C.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -179,6 +188,19 @@ def lib() -> C.CDLL:
         L.psc_classify_host.argtypes = [P, P, P, P, I32, P]
         L.psc_class_mask_host.argtypes = [P, I32, P]
         L.psc_host_state.argtypes = [P, C.c_char_p, C.c_size_t, P, P, I32, P]
+        L.psc_device_bytes_ex.argtypes = [P, C.c_uint32]
+        L.psc_device_bytes_ex.restype = C.c_size_t
+        L.psc_bind_device_ex.argtypes = [P, P, C.c_size_t, C.c_uint32, P]
+        L.psc_compute_masks_n.argtypes = [P, P, I64, P, P, I32, P, P]
+        L.psc_compute_classes_n.argtypes = [P, P, I64, P, P, I32, P, P]
+        L.psc_compute_and_apply_n.argtypes = [P, P, I64, P, P, I32, P, P, C.c_int, I32, P]
+        L.psc_compute_and_argmax_n.argtypes = [P, P, I64, P, P, I32, P, C.c_int, I32, P, P]
+        L.psc_predictor_fill.argtypes = [P, I32, P]
+        L.psc_set_options.argtypes = [P, C.c_uint32]
+        L.psc_predictor_updates.argtypes = [P, P, I32, P]
+        L.psc_timeline_records.argtypes = [P, I32, C.c_int]
+        L.psc_timeline_records.restype = I64
+        L.psc_compute_and_apply_timeline.argtypes = [P, P, I64, P, P, I32, P, P, C.c_int, I32, P, I64, P]
         L.psc_free.argtypes = [P]
         L.psc_free.restype = None
         L.psc_last_error.restype = C.c_char_p
@@ -186,7 +208,10 @@ def lib() -> C.CDLL:
                      "psc_compute_and_apply", "psc_state_reset", "psc_advance", "psc_compute_masks_dense",
                      "psc_compute_and_apply_dense", "psc_compute_and_argmax", "psc_compute_and_argmax_dense",
                      "psc_compute_classes", "psc_compute_classes_dense", "psc_decode_step", "psc_save", "psc_load", "psc_device_error_count",
-                     "psc_classify_host", "psc_class_mask_host", "psc_host_state"):
+                     "psc_classify_host", "psc_class_mask_host", "psc_host_state", "psc_bind_device_ex",
+                     "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n",
+                     "psc_compute_and_argmax_n", "psc_predictor_fill", "psc_predictor_updates",
+                     "psc_compute_and_apply_timeline", "psc_set_options"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -308,17 +333,57 @@ class Classifier:
         return out
 
     # -------------------------------------------------------------- device
-    def bind(self, device="cuda", stream=None):
+    def bind(self, device="cuda", stream=None, layout=None):
+        """Copy the tables to `device`; layout "flat" or "sliced" chooses the
+        mask table's layout (psc_bind_device_ex), None the library default."""
         import torch
-        n = int(lib().psc_device_bytes(self._h))
+        _require(layout in _LAYOUTS, "layout None, 'flat' or 'sliced'")
+        flags = _LAYOUTS[layout]
+        n = int(lib().psc_device_bytes_ex(self._h, flags))
         buf = torch.empty(n + 256, dtype=torch.uint8, device=device)
         off = (-buf.data_ptr()) % 256
+        ptr = buf.data_ptr() + off
+        _check(lib().psc_bind_device_ex(self._h, ptr, n, flags, _stream_ptr(stream)))
         self._dev = buf
         self._device = buf.device
         self._dev_index = buf.get_device()
-        self._dev_ptr = buf.data_ptr() + off
-        _check(lib().psc_bind_device(self._h, self._dev_ptr, n, _stream_ptr(stream)))
+        self._dev_ptr = ptr
         return self
+
+    def set_options(self, speculate: bool = False):
+        """psc_set_options: PSC_OPT_SPECULATE when `speculate`."""
+        _check(lib().psc_set_options(self._h, OPT_SPECULATE if speculate else 0))
+        return self
+
+    def predictor_fill(self, cls: int = -1, stream=None):
+        """Every class-predictor entry to `cls` (-1: no prediction)."""
+        _check(lib().psc_predictor_fill(self._h, int(cls), _stream_ptr(stream)))
+
+    def predictor_updates(self, reset: bool = False, stream=None) -> int:
+        """Walks whose class differed from the prediction since the last reset."""
+        v = C.c_uint32()
+        _check(lib().psc_predictor_updates(self._h, C.byref(v), int(reset), _stream_ptr(stream)))
+        return int(v.value)
+
+    def timeline_records(self, B: int, dtype) -> int:
+        code = (_T or _torch_types())["codes"][dtype]
+        return int(lib().psc_timeline_records(self._h, int(B), code))
+
+    def compute_and_apply_timeline(self, stacks, stack_lens, lexer_states, logits, records, out=None, stream=None):
+        """psc_compute_and_apply_timeline: the fused step with per-wavefront
+        clock records (records: int64 device tensor [n, 4])."""
+        B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out, self.W)
+        T = _T or _torch_types()
+        import torch
+        _require(isinstance(records, T["tensor"]) and records.dtype == torch.int64 and records.is_contiguous()
+                 and records.dim() == 2 and records.shape[1] == 4 and records.get_device() == self._idx,
+                 "records as a contiguous int64 device tensor [n, 4]")
+        out_ptr = None if out is None else out.data_ptr()
+        _check(lib().psc_compute_and_apply_timeline(self._h, stacks.data_ptr(), stacks.numel(),
+                                                    stack_lens.data_ptr(), lexer_states.data_ptr(), B, out_ptr,
+                                                    logits.data_ptr(), dt, self.V, records.data_ptr(),
+                                                    records.shape[0], _stream_ptr(stream)))
+        return logits
 
     @property
     def device(self):
@@ -341,8 +406,8 @@ class Classifier:
         if out is None:
             out = torch.empty((int(stack_lens.shape[0]), self.W), dtype=torch.int32, device=self.device)
         B, _ = _step_args(self._idx, stacks, stack_lens, lexer_states, out=out, out_cols=self.W)
-        _check(lib().psc_compute_masks(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
-                                       lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
+        _check(lib().psc_compute_masks_n(self._h, stacks.data_ptr(), stacks.numel(), stack_lens.data_ptr(),
+                                         lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
 
     def compute_classes(self, stacks, stack_lens, lexer_states, out=None, stream=None):
@@ -351,8 +416,8 @@ class Classifier:
         if out is None:
             out = torch.empty(int(stack_lens.shape[0]), dtype=torch.int32, device=self.device)
         B, _ = _step_args(self._idx, stacks, stack_lens, lexer_states, out=out)
-        _check(lib().psc_compute_classes(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
-                                         lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
+        _check(lib().psc_compute_classes_n(self._h, stacks.data_ptr(), stacks.numel(), stack_lens.data_ptr(),
+                                           lexer_states.data_ptr(), B, out.data_ptr(), _stream_ptr(stream)))
         return out
 
     def compute_and_apply(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
@@ -360,9 +425,9 @@ class Classifier:
         place; the bitmask is also written to `out` when given.  Returns logits."""
         B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out, self.W)
         out_ptr = None if out is None else out.data_ptr()
-        _check(lib().psc_compute_and_apply(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
-                                           lexer_states.data_ptr(), B, out_ptr, logits.data_ptr(), dt,
-                                           self.V, _stream_ptr(stream)))
+        _check(lib().psc_compute_and_apply_n(self._h, stacks.data_ptr(), stacks.numel(), stack_lens.data_ptr(),
+                                             lexer_states.data_ptr(), B, out_ptr, logits.data_ptr(), dt,
+                                             self.V, _stream_ptr(stream)))
         return logits
 
     def compute_and_argmax(self, stacks, stack_lens, lexer_states, logits, out=None, stream=None):
@@ -372,9 +437,9 @@ class Classifier:
         if out is None:
             out = torch.empty(int(stack_lens.shape[0]), dtype=torch.int32, device=self.device)
         B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out)
-        _check(lib().psc_compute_and_argmax(self._h, stacks.data_ptr(), stack_lens.data_ptr(),
-                                            lexer_states.data_ptr(), B, logits.data_ptr(), dt, self.V,
-                                            out.data_ptr(), _stream_ptr(stream)))
+        _check(lib().psc_compute_and_argmax_n(self._h, stacks.data_ptr(), stacks.numel(), stack_lens.data_ptr(),
+                                              lexer_states.data_ptr(), B, logits.data_ptr(), dt, self.V,
+                                              out.data_ptr(), _stream_ptr(stream)))
         return out
 
     def error_count(self, reset: bool = False, stream=None) -> int:

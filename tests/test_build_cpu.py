@@ -60,6 +60,17 @@ def test_info_is_consistent():
     assert inf["mask_stride_words"] % 64 == 0 and inf["mask_stride_words"] >= inf["mask_words"]
     assert inf["dfa_states"] <= inf["dfa_states_built"]
     assert inf["device_bytes"] >= inf["table_bytes"] + inf["mask_table_bytes"]
+    # the sliced layout: distinct 64-word slices plus one id per (row, slice)
+    n_slices = inf["mask_stride_words"] // 64
+    assert inf["sliced_mask_bytes"] == 4 * (64 * inf["mask_slices_unique"] + inf["n_classes"] * n_slices)
+    assert 1 <= inf["mask_slices_unique"] <= inf["n_classes"] * n_slices
+    assert inf["sliced_mask_bytes"] < inf["mask_table_bytes"]
+    assert inf["bound_mask_layout"] == 0
+    clf = Classifier(wl.grammar, wl.vocab)
+    lib = psc.lib()
+    flat, sliced = (lib.psc_device_bytes_ex(clf._h, f) for f in (psc.BIND_FLAT, psc.BIND_SLICED))
+    assert flat == lib.psc_device_bytes(clf._h) == lib.psc_device_bytes_ex(clf._h, 0)
+    assert flat - sliced >= inf["mask_table_bytes"] - inf["sliced_mask_bytes"] - 512
 
 
 def test_host_walk_range_faults():
