@@ -376,6 +376,7 @@ struct Builder {
     std::vector<std::vector<int32_t>> goto_sources;  // per nonterminal
     int64_t states_built = 0;
     std::atomic<int64_t> *total_states = nullptr;
+    int64_t max_states = 60'000'000;   // over all lexer states; PSC_BUILD_MAX_STATES overrides
 
     // per-q: trie of realizable terminal sequences
     std::vector<int32_t> tn_label, tn_child_beg, tn_child_end, tn_children, tn_grp_beg, tn_grp_end, tn_grps;
@@ -659,8 +660,9 @@ struct Builder {
             qs_eend.push_back(0);
             queue.push_back(id);
             states_built++;
-            if (total_states && total_states->fetch_add(1) + 1 > 60'000'000)
-                throw BuildError(PSC_E_LIMIT, "automaton exceeds 60M states");
+            if (total_states && total_states->fetch_add(1) + 1 > max_states)
+                throw BuildError(PSC_E_LIMIT, "automaton exceeds " + std::to_string(max_states) +
+                                                  " states (PSC_BUILD_MAX_STATES)");
         }
         return id;
     }
@@ -1114,6 +1116,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             try {
                 Builder &Bt = *builders[t];
                 Bt.total_states = &total_states;
+                if (const char *e = std::getenv("PSC_BUILD_MAX_STATES")) Bt.max_states = std::atoll(e);
                 for (int32_t q; (q = next_q.fetch_add(1)) < G.nQ;) Bt.build_for_lexer_state(q);
             } catch (...) {
                 errs[t] = std::current_exception();
