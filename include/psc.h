@@ -452,6 +452,23 @@ psc_status psc_decode_step(const psc_handle *h, const int32_t *stacks_in, const 
                            int32_t cap, int32_t B, const int32_t *tokens, int32_t *status,
                            uint32_t *out_bitmask, void *logits, psc_dtype dtype, int32_t V, void *stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * results as psc_compute_and_argmax_n, with the per-sequence argmax records
+ * in a fixed array of the library's own (one copy per GPU, 512 KiB, taken
+ * and cleared by the first psc_bind_device on that GPU and held until the
+ * process ends) instead of the bound buffer.  The call allocates nothing.
+ * B <= 4096, else PSC_E_INVALID_ARG.  Every call on one GPU shares that
+ * GPU's array (through any handle): calls that overlap in time on one GPU
+ * race and give wrong tokens; each completed call leaves the array zeroed.
+ * Errors: PSC_E_INVALID_ARG, PSC_E_NOT_BOUND, PSC_E_DEVICE.
+ */
+psc_status psc_compute_and_argmax_noalloc(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,
+                                          const void *logits, psc_dtype dtype, int32_t V, int32_t *out_tokens,
+                                          void *stream);
+
 /* psc_compute_and_argmax on device-resident states (dense layout above). */
 psc_status psc_compute_and_argmax_dense(const psc_handle *h, const int32_t *stacks, int32_t cap,
                                         const int32_t *stack_lens, const int32_t *lexer_states, int32_t B,

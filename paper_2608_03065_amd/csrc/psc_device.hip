@@ -11,7 +11,9 @@
 // the application is a pure HBM stream.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -990,6 +992,22 @@ argmax_partial_kernel(const int32_t *__restrict__ table, const uint32_t *__restr
     }
 }
 
+// ---------------------------------------------------------------- allocation-free argmax records
+
+// The argmax slot records of psc_compute_and_argmax_noalloc: a fixed array
+// in the library's own device memory, one copy per GPU, held until the
+// process ends (kScratchSeqs records of 128 bytes: 512 KiB).  Host code
+// never uses this name as an address (it is a host-side stand-in there):
+// it uses the per-device address that hipGetSymbolAddress returns.
+constexpr int32_t kScratchSeqs = 4096;
+static __device__ __align__(256) unsigned long long scratch[kScratchSeqs * kArgmaxRecordWords];
+
+// Zero n uint64 words (the records' state between calls), with vector stores.
+__global__ void __launch_bounds__(kBlock)
+zero_words_kernel(unsigned long long *__restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) p[i] = 0;
+}
+
 // ---------------------------------------------------------------- advance
 
 // The problem instance on the device (the lexing and parsing steps of
@@ -1483,9 +1501,12 @@ psc_status launch_fused(const psc_handle *h, const int32_t *stacks, int32_t stri
 }
 
 // The masked argmax for ragged (stride 0) or strided stacks.
+// `records` is the per-sequence slot array (kArgmaxRecordWords uint64 per
+// sequence, zero between calls); null selects the bound buffer's.
 psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t stride, int64_t n_stack,
                          const int32_t *stack_lens, const int32_t *lexer_states, int32_t B, const void *logits,
-                         psc_dtype dtype, int32_t V, int32_t *out_tokens, void *stream, const char *what) {
+                         psc_dtype dtype, int32_t V, int32_t *out_tokens, void *stream, const char *what,
+                         unsigned long long *records = nullptr) {
     if (psc_status st = check_states(h, stacks, stride, n_stack, stack_lens, lexer_states, B, out_tokens, what))
         return st;
     if (psc_status st = check_logits(h, logits, dtype, V, B, what)) return st;
@@ -1497,7 +1518,7 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
     const int32_t W = h->W;
     const int words_per_block = !fast ? kGenWords : fused_words_per_block(dtype == PSC_BF16);
     dim3 grid((W + words_per_block - 1) / words_per_block, B);
-    auto *records = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
+    if (!records) records = reinterpret_cast<unsigned long long *>(base + h->argmax_off);
 #define PSC_ARGMAX(BF, SL)                                                                                           \
     hipLaunchKernelGGL((argmax_partial_kernel<BF, SL>), grid, dim3(kFusedBlock), 0, s, T.table, T.masks, T.mstride,   \
                        T.ids, h->n_lex, h->n_lr, stacks, stride, n_stack, stack_lens, lexer_states, V, W, T.err,    \
@@ -1508,6 +1529,28 @@ psc_status launch_argmax(const psc_handle *h, const int32_t *stacks, int32_t str
     else PSC_ARGMAX(false, false);
 #undef PSC_ARGMAX
     return launched(what);
+}
+
+// Per-device address of `scratch`, taken once per device (at the first
+// bind on it, with that device current) and cleared there; null until then.
+constexpr int kMaxDevices = 64;
+std::atomic<unsigned long long *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+hipError_t scratch_setup(int device, hipStream_t s) {
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch[device].load(std::memory_order_acquire)) return hipSuccess;
+    void *ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)kScratchSeqs * kArgmaxRecordWords;
+    hipLaunchKernelGGL(zero_words_kernel, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, s,
+                       static_cast<unsigned long long *>(ptr), n);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) g_scratch[device].store(static_cast<unsigned long long *>(ptr), std::memory_order_release);
+    return e;
 }
 
 constexpr int64_t kUnbounded = INT64_MAX;
@@ -1605,7 +1648,11 @@ extern "C" psc_status psc_bind_device_ex(psc_handle *h, void *dev_buf, size_t nb
     if (e == hipSuccess)
         e = hipMemsetAsync(base + L.pred, 0xFF, (size_t)start_block_count(h->n_lex) * kPredInts * sizeof(int32_t), s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
+    int device = -1;
+    if (e == hipSuccess) e = hipGetDevice(&device);
+    if (e == hipSuccess) e = scratch_setup(device, s);
     if (e != hipSuccess) return device_fail("psc_bind_device", e);
+    h->device = device;
     h->dev_base = dev_buf;
     h->dev_bytes = nbytes;
     h->sliced = L.sliced;
@@ -1739,6 +1786,27 @@ extern "C" psc_status psc_compute_and_argmax_dense(const psc_handle *h, const in
         return st;
     return launch_argmax(h, stacks, cap, kUnbounded, stack_lens, lexer_states, B, logits, dtype, V, out_tokens,
                          stream, "psc_compute_and_argmax_dense");
+}
+
+extern "C" psc_status psc_compute_and_argmax_noalloc(const psc_handle *h, const int32_t *stacks, int64_t n_stack,
+                                                    const int32_t *stack_lens, const int32_t *lexer_states,
+                                                    int32_t B, const void *logits, psc_dtype dtype, int32_t V,
+                                                    int32_t *out_tokens, void *stream) {
+    const char *what = "psc_compute_and_argmax_noalloc";
+    if (psc_status st = check_bound(h, what)) return st;
+    if (B > kScratchSeqs) {
+        set_error(std::string(what) + ": B > " + std::to_string(kScratchSeqs) +
+                  " (the fixed record array holds that many sequences)");
+        return PSC_E_INVALID_ARG;
+    }
+    unsigned long long *records =
+        h->device >= 0 && h->device < kMaxDevices ? g_scratch[h->device].load(std::memory_order_acquire) : nullptr;
+    if (!records) {
+        set_error(std::string(what) + ": no record array on the bound device");
+        return PSC_E_NOT_BOUND;
+    }
+    return launch_argmax(h, stacks, 0, n_stack, stack_lens, lexer_states, B, logits, dtype, V, out_tokens, stream,
+                         what, records);
 }
 
 extern "C" psc_status psc_set_options(psc_handle *h, uint32_t options) {

@@ -127,6 +127,7 @@ struct psc_handle {
     // device binding (caller-owned memory)
     void *dev_base = nullptr;
     size_t dev_bytes = 0;
+    int device = -1;               // the HIP device current at bind time
     size_t mask_off = 0, ids_off = 0, gram_off = 0, vbytes_off = 0, argmax_off = 0, packed_off = 0,
            closure_off = 0, pred_off = 0;
     bool sliced = false;           // the bound mask table is the sliced layout

@@ -28,7 +28,7 @@ EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc
             "psc_host_state", "psc_free", "psc_last_error", "psc_device_bytes_ex", "psc_bind_device_ex",
             "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n", "psc_compute_and_argmax_n",
             "psc_predictor_fill", "psc_predictor_updates", "psc_timeline_records", "psc_compute_and_apply_timeline",
-            "psc_set_options"]
+            "psc_set_options", "psc_compute_and_argmax_noalloc"]
 
 BIND_FLAT, BIND_SLICED = 1, 2
 OPT_SPECULATE = 1
@@ -195,6 +195,7 @@ def lib() -> C.CDLL:
         L.psc_compute_classes_n.argtypes = [P, P, I64, P, P, I32, P, P]
         L.psc_compute_and_apply_n.argtypes = [P, P, I64, P, P, I32, P, P, C.c_int, I32, P]
         L.psc_compute_and_argmax_n.argtypes = [P, P, I64, P, P, I32, P, C.c_int, I32, P, P]
+        L.psc_compute_and_argmax_noalloc.argtypes = [P, P, I64, P, P, I32, P, C.c_int, I32, P, P]
         L.psc_predictor_fill.argtypes = [P, I32, P]
         L.psc_set_options.argtypes = [P, C.c_uint32]
         L.psc_predictor_updates.argtypes = [P, P, I32, P]
@@ -211,7 +212,7 @@ def lib() -> C.CDLL:
                      "psc_classify_host", "psc_class_mask_host", "psc_host_state", "psc_bind_device_ex",
                      "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n",
                      "psc_compute_and_argmax_n", "psc_predictor_fill", "psc_predictor_updates",
-                     "psc_compute_and_apply_timeline", "psc_set_options"):
+                     "psc_compute_and_apply_timeline", "psc_set_options", "psc_compute_and_argmax_noalloc"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -440,6 +441,17 @@ class Classifier:
         _check(lib().psc_compute_and_argmax_n(self._h, stacks.data_ptr(), stacks.numel(), stack_lens.data_ptr(),
                                               lexer_states.data_ptr(), B, logits.data_ptr(), dt, self.V,
                                               out.data_ptr(), _stream_ptr(stream)))
+        return out
+
+    def compute_and_argmax_noalloc(self, stacks, stack_lens, lexer_states, logits, out, stream=None):
+        """compute_and_argmax whose records live in the library's fixed
+        per-GPU array (the call allocates nothing; B <= 4096; calls on one
+        GPU must not overlap).  `out` is required: int32 [B]."""
+        B, dt = _step_args(self._idx, stacks, stack_lens, lexer_states, logits, self.V, out)
+        _check(lib().psc_compute_and_argmax_noalloc(self._h, stacks.data_ptr(), stacks.numel(),
+                                                    stack_lens.data_ptr(), lexer_states.data_ptr(), B,
+                                                    logits.data_ptr(), dt, self.V, out.data_ptr(),
+                                                    _stream_ptr(stream)))
         return out
 
     def error_count(self, reset: bool = False, stream=None) -> int:
