@@ -142,7 +142,12 @@ enum { PSC_BIND_FLAT = 1, PSC_BIND_SLICED = 2 };
  * and flattens everything into device-ready arrays.
  * On success *out receives a new handle.  Errors: PSC_E_INVALID_ARG (null
  * pointers, sizes <= 0), PSC_E_GRAMMAR (ids out of range, a non-EOS token with
- * an empty spelling), PSC_E_OOM, PSC_E_LIMIT.
+ * an empty spelling), PSC_E_OOM, PSC_E_LIMIT (more subset states built, over
+ * all lexer states and before minimisation, than the environment variable
+ * PSC_BUILD_MAX_STATES allows; default 10^9).  The construction runs on as
+ * many threads as the process's CPU affinity mask holds, at most
+ * OMP_NUM_THREADS when that is set and at most 32; PSC_BUILD_THREADS
+ * overrides.
  */
 psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out);
 

@@ -1,4 +1,4 @@
-"""The five synthetic workloads (grammar, vocabulary, prefixes, logits).
+"""The six synthetic workloads (grammar, vocabulary, prefixes, logits).
 
 Each prefix is drawn independently per (step, b) from a seeded random
 document of the workload's language, truncated at a uniform byte position
@@ -13,7 +13,7 @@ from typing import Callable
 
 import numpy as np
 
-from . import documents, grammars, pylike, schema, vocab
+from . import documents, grammars, gosql, pylike, schema, vocab
 from .grammar import GrammarTables
 from .native import HostParser
 from .seeds import rng_for
@@ -21,7 +21,7 @@ from .seeds import rng_for
 
 @dataclass
 class Workload:
-    index: int                   # 0..4
+    index: int                   # 0..5
     name: str
     B: int
     steps: int
@@ -184,6 +184,22 @@ STRESS = _register(_DeepWorkload(
     4, "stress", B=256, steps=1000, logits_dtype="bf16", logits_std=2.0,
     make_grammar=pylike.grammar, make_vocab=_c5_vocab, make_document=_c5_doc, doc_pool=256,
     description="Python-like CFG, deep nesting (stack depth ~ U{1..1000}); V=262,144; B=256; bf16 N(0,2)"))
+
+
+def _c6_vocab(g):
+    return gosql.gosql_vocab(rng_for(5, salt=0x70C), 4096)
+
+
+def _c6_doc(rng, wl):
+    return gosql.document(rng)
+
+
+GOSQL = _register(Workload(
+    5, "gosql", B=128, steps=500, logits_dtype="bf16", logits_std=2.0,
+    make_grammar=gosql.grammar, make_vocab=_c6_vocab, make_document=_c6_doc, doc_pool=1024,
+    description="Go-like language with embedded SQL (296 terminals, 255 nonterminals, 1504 LALR(1) states); "
+                "a quarter of the documents nest without closing (stack depth p90 ~200, max ~640); "
+                "V=4,096; B=128; bf16 N(0,2)"))
 
 
 def get(name: str) -> Workload:

@@ -42,6 +42,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <sched.h>
 #include <stdexcept>
 #include <system_error>
 #include <unordered_map>
@@ -376,7 +377,7 @@ struct Builder {
     std::vector<std::vector<int32_t>> goto_sources;  // per nonterminal
     int64_t states_built = 0;
     std::atomic<int64_t> *total_states = nullptr;
-    int64_t max_states = 60'000'000;   // over all lexer states; PSC_BUILD_MAX_STATES overrides
+    int64_t max_states = 1'000'000'000;   // built over all lexer states; PSC_BUILD_MAX_STATES overrides
 
     // per-q: trie of realizable terminal sequences
     std::vector<int32_t> tn_label, tn_child_beg, tn_child_end, tn_children, tn_grp_beg, tn_grp_end, tn_grps;
@@ -1101,7 +1102,15 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         bool verbose = std::getenv("PSC_BUILD_VERBOSE") != nullptr;
         Completions C = completions(G);
         VocabTrie VT = vocab_trie(vocab);
+        // the CPUs this process may run on (its affinity mask), capped by
+        // OMP_NUM_THREADS when that is set; PSC_BUILD_THREADS overrides both
         int32_t n_threads = (int32_t)std::thread::hardware_concurrency();
+        cpu_set_t cpus;
+        if (sched_getaffinity(0, sizeof(cpus), &cpus) == 0) n_threads = CPU_COUNT(&cpus);
+        if (const char *e = std::getenv("OMP_NUM_THREADS")) {
+            const int k = std::atoi(e);
+            if (k > 0) n_threads = std::min(n_threads, k);
+        }
         if (const char *e = std::getenv("PSC_BUILD_THREADS")) n_threads = std::atoi(e);
         n_threads = std::max(1, std::min({n_threads, 32, G.nQ}));
         std::vector<std::unique_ptr<Builder>> builders;

@@ -1,6 +1,6 @@
 """Every decoding step of the three smaller workloads through both step forms
 at the benchmarked shape, against the oracle; twenty sampled steps of each
-larger one.
+programming-language workload.
 
 PSC computes exactly the set of eq. simp (Theorems 1-3), so the bar is bit
 equality with the oracle on every row of every step (Algorithm 2: the
@@ -91,7 +91,7 @@ def test_every_step_bit_exact_speculative(built, name):
         clf.predictor_fill(-1)
 
 
-@pytest.mark.parametrize("name", ["pylike", "stress"])
+@pytest.mark.parametrize("name", ["pylike", "stress", "gosql"])
 def test_twenty_sampled_steps_bit_exact(built, name):
     wl = built(name)[0]
     steps = np.linspace(0, wl.steps - 1, 20).astype(int).tolist()

@@ -80,7 +80,7 @@ def _check_step(clf, wl, orc, states, step, ref_classes=None):
 
 
 @pytest.mark.parametrize("name,steps", [("arithmetic", [0, 9]), ("json", [3, 250]), ("schema", [5, 640]),
-                                        ("pylike", [7, 321]), ("stress", [17])])
+                                        ("pylike", [7, 321]), ("stress", [17]), ("gosql", [4, 333])])
 def test_sliced_layout_bit_exact(built, name, steps):
     wl, clf, orc = built(name)
     sl = _sliced(built, name)
