@@ -327,6 +327,16 @@ def main():
         t_fill = graph_loop(fill)
         t_copy = graph_loop(copy)
 
+        # the apply kernel's floors at this shape: an all-zero bitmask (every
+        # vector one store of -inf, no logits read) and an all-one bitmask
+        # (no logits touched: the launch and the bitmask read); beside
+        # apply_mask_solo they show what reading the mixed vectors costs
+        bm_const = {"all_masked": torch.zeros((B, W), dtype=torch.int32, device=dev),
+                    "all_allowed": torch.full((B, W), -1, dtype=torch.int32, device=dev)}
+        t_apply_floor = {}
+        for name_, bm_c in bm_const.items():
+            t_apply_floor[name_] = round(loop(lambda i: apply_mask(pool[i % n_pool], bm_c, stream=stream), 1000), 3)
+
         tl = None
         if args.timeline > 0:
             tl = timeline(clf, wl, step_inputs, pool, bms, stream, dev, args.timeline, prequeue)
@@ -468,6 +478,8 @@ def main():
                                 "bench stream before the step; PCIe-inclusive, not the headline"},
         "graph_step_us": round(t_graph, 3),
         "kernels_us": {"compute_masks_solo": round(t_compute, 3), "apply_mask_solo": round(t_apply, 3),
+                       "apply_mask_all_masked": t_apply_floor["all_masked"],
+                       "apply_mask_all_allowed": t_apply_floor["all_allowed"],
                        "apply_mask_solo_gbs": round(achieved_apply, 1),
                        "compute_masks_solo_graph": round(t_compute_graph, 3),
                        "apply_mask_solo_graph": round(t_apply_graph, 3)},

@@ -143,6 +143,10 @@ def _c4_vocab(g):
 
 
 def _c4_doc(rng, wl):
+    # one document in four nests without closing, so that prefixes reach
+    # stack depths up to about 200
+    if rng.random() < 0.25:
+        return pylike.deep_program(rng, approx_chars=int(rng.integers(150, 520)))
     return pylike.program(rng)
 
 
@@ -150,6 +154,7 @@ PYLIKE = _register(Workload(
     3, "pylike", B=128, steps=500, logits_dtype="bf16", logits_std=2.0,
     make_grammar=pylike.grammar, make_vocab=_c4_vocab, make_document=_c4_doc, doc_pool=2048,
     description="Python-like CFG (88 terminals, 14 binary precedence levels, INDENT/DEDENT); "
+                "a quarter of the documents nest without closing (stack depth up to ~200); "
                 "V=128,256; B=128; bf16 N(0,2)"))
 
 
