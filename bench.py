@@ -338,7 +338,9 @@ def main():
             t_apply_floor[name_] = round(loop(lambda i: apply_mask(pool[i % n_pool], bm_c, stream=stream), 1000), 3)
 
         tl = None
-        if args.timeline > 0:
+        if args.timeline > 0 and V % 32 != 0:
+            tl = {"skipped": "the timeline records come from the fast path of the fused step (V % 32 == 0)"}
+        elif args.timeline > 0:
             tl = timeline(clf, wl, step_inputs, pool, bms, stream, dev, args.timeline, prequeue)
 
         # (4) Algorithm 2 entirely on the GPU: device-resident prefix states
