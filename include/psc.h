@@ -35,7 +35,9 @@ extern "C" {
 typedef enum {
     PSC_OK = 0,
     PSC_E_INVALID_ARG = -1, /* null pointer, negative size, inconsistent shape */
-    PSC_E_GRAMMAR = -2,     /* malformed tables (ids out of range, empty spelling, ...) */
+    PSC_E_GRAMMAR = -2,     /* malformed tables (ids out of range, empty spelling, ...)
+                               or grammar text (syntax, undefined symbol, ...)          */
+    PSC_E_NOT_LALR1 = -3,   /* psc_grammar_compile: the grammar has LALR(1) conflicts  */
     PSC_E_OOM = -4,         /* host allocation failed (memory or threads)             */
     PSC_E_DEVICE = -5,      /* a HIP call or kernel launch failed                     */
     PSC_E_NOT_BOUND = -6,   /* device tables not bound (psc_bind_device)              */
@@ -150,6 +152,46 @@ enum { PSC_BIND_FLAT = 1, PSC_BIND_SLICED = 2 };
  * overrides.
  */
 psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_handle **out);
+
+/*
+ * Grammar text -> the tables psc_build takes (T and P, the arguments of
+ * Algorithm 1; Sec. 4.1 obtains P from an LALR(1) generator).  One statement
+ * per line, '#' starts a comment outside quotes and slashes:
+ *   %start NAME                the start nonterminal
+ *   %ignore NAME /regex/       a terminal the lexer consumes and drops
+ *   %literal "text" [PRIO]     declare a literal terminal at this point
+ *   NAME[.PRIO]: /regex/       a regex terminal
+ *   name: item item | item     productions of `name`; an item is a declared
+ *                              terminal, a "literal" (declared on first use)
+ *                              or a nonterminal; '|' separates alternatives,
+ *                              an empty one is the empty production, and a
+ *                              line starting with '|' continues the rule.
+ * Literals take \\ \" \n \t \r \xHH.  Regexes are over bytes: . [...] [^...]
+ * ( ) (?: ) | * + ? {m} {m,} {m,n} and \n \t \r \f \v \0 \xHH \d \w \s;
+ * another escaped byte stands for itself (\/ is a slash).
+ * Lexing is longest match with one byte of lookahead; a tie on the same
+ * lexeme goes to the higher priority, then a literal over a regex, then the
+ * earlier declaration.  Terminal ids follow declaration order, then $END;
+ * nonterminal ids follow first appearance as a left side, then $start;
+ * production 0 is $start -> start.  The LR(1) tables are LALR(1), built from
+ * the LR(0) automaton with DeRemer-Pennello lookaheads; nothing is resolved
+ * by precedence and no reduction is defaulted.
+ * On success *out owns the tables (psc_grammar_free).  Errors:
+ * PSC_E_INVALID_ARG, PSC_E_GRAMMAR (syntax, undefined or misused symbol, a
+ * terminal matching the empty string; the message names the line),
+ * PSC_E_NOT_LALR1 (the message names the first conflicts: state, terminal
+ * and the two actions), PSC_E_OOM.
+ */
+typedef struct psc_compiled_grammar psc_compiled_grammar;
+psc_status psc_grammar_compile(const char *text, size_t len, psc_compiled_grammar **out);
+/* The tables as the psc_grammar that psc_build takes; the pointers stay valid
+ * until psc_grammar_free. */
+psc_status psc_grammar_view(const psc_compiled_grammar *g, psc_grammar *out);
+/* Name of terminal id (terminal != 0) or nonterminal id; NULL out of range. */
+const char *psc_grammar_symbol_name(const psc_compiled_grammar *g, int32_t terminal, int32_t id);
+void psc_grammar_free(psc_compiled_grammar *g);
+/* psc_grammar_compile, then psc_build on the result. */
+psc_status psc_build_from_text(const char *text, size_t len, const psc_vocab *vocab, psc_handle **out);
 
 /*
  * Persistence of a built classifier, so that Algorithm 1 runs once per

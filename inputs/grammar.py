@@ -55,6 +55,7 @@ class GrammarTables:
     prod_lhs: np.ndarray              # int32 [n_productions]
     prod_len: np.ndarray              # int32 [n_productions]
     productions: list[tuple[str, tuple[str, ...]]] = field(default_factory=list)
+    text: str = ""                    # the grammar in the C library's text form (Grammar.to_text)
 
     @property
     def n_terminals(self) -> int:
@@ -92,11 +93,11 @@ class Grammar:
     def regex(self, name: str, pattern: str, priority: int = 0) -> str:
         if name in self._term_index:
             raise GrammarError(f"terminal {name} declared twice")
-        self._add_term(TerminalDef(name, parse_regex(pattern), priority, False, False))
+        self._add_term(TerminalDef(name, parse_regex(pattern), priority, False, False, pattern))
         return name
 
     def ignore(self, name: str, pattern: str) -> str:
-        self._add_term(TerminalDef(name, parse_regex(pattern), 0, False, True))
+        self._add_term(TerminalDef(name, parse_regex(pattern), 0, False, True, pattern))
         return name
 
     def _add_term(self, t: TerminalDef):
@@ -146,6 +147,37 @@ class Grammar:
         m = self.fresh("sepopt")
         self.rule(m, [], [n])
         return m
+
+    # ----- text form ---------------------------------------------------------
+    def to_text(self) -> str:
+        """The grammar in the text form that the C library compiles
+        (psc_grammar_compile): every terminal declared in this builder's
+        order, so that both front ends number terminals, nonterminals and
+        productions alike."""
+        out = [f"%start {self.start}"]
+        for t in self._terms:
+            if t.is_literal:
+                lit = _escape_literal(t.name[1:-1])
+                out.append(f"%literal {lit} {t.priority}" if t.priority else f"%literal {lit}")
+            else:
+                _check_name(t.name)
+                pat = "/" + _escape_regex(t.pattern) + "/"
+                if t.ignored:
+                    out.append(f"%ignore {t.name} {pat}")
+                else:
+                    out.append(f"{t.name}.{t.priority}: {pat}" if t.priority else f"{t.name}: {pat}")
+        for lhs, body in self._rules:
+            _check_name(lhs)
+            items = []
+            for sym in body:
+                t = self._term_index.get(sym)
+                if t is not None and self._terms[t].is_literal:
+                    items.append(_escape_literal(sym[1:-1]))
+                else:
+                    _check_name(sym)
+                    items.append(sym)
+            out.append(f"{lhs}: " + " ".join(items) if items else f"{lhs}:")
+        return "\n".join(out) + "\n"
 
     # ----- compile ---------------------------------------------------------
     def compile(self) -> GrammarTables:
@@ -198,7 +230,49 @@ class Grammar:
             prod_lhs=np.array([p[0] for p in prods], dtype=np.int32),
             prod_len=np.array([len(p[1]) for p in prods], dtype=np.int32),
             productions=names,
+            text=self.to_text(),
         )
+
+
+def _check_name(name: str):
+    if not name or not all(c.isascii() and (c.isalnum() or c in "_$") for c in name):
+        raise GrammarError(f"{name!r} cannot be written in the text form")
+
+
+def _escape_literal(text: str) -> str:
+    out = []
+    for ch in text:
+        o = ord(ch)
+        if ch in '"\\':
+            out.append("\\" + ch)
+        elif 0x20 <= o < 0x7F:
+            out.append(ch)
+        else:
+            out.append(f"\\x{o:02x}")
+    return '"' + "".join(out) + '"'
+
+
+def _escape_regex(pattern: str) -> str:
+    """Bytes outside printable ASCII as \\xHH and a bare '/' as '\\/'; an
+    escape sequence of the pattern is kept as it is."""
+    out = []
+    i = 0
+    while i < len(pattern):
+        ch = pattern[i]
+        if ch == "\\" and i + 1 < len(pattern):
+            nxt = pattern[i + 1]
+            out.append("\\" + nxt if 0x20 <= ord(nxt) < 0x7F else f"\\x{ord(nxt):02x}")
+            i += 2
+            continue
+        o = ord(ch)
+        if ch == "/":
+            out.append("\\/")
+        elif 0x20 <= o < 0x7F:
+            out.append(ch)
+        else:
+            out.append(f"\\x{o:02x}")
+        i += 1
+    return "".join(out)
 
 
 # --------------------------------------------------------------------------

@@ -258,6 +258,7 @@ class TerminalDef:
     priority: int = 0
     is_literal: bool = False
     ignored: bool = False
+    pattern: str = ""          # the regex text (regex terminals)
 
 
 @dataclass

@@ -34,11 +34,13 @@ def build(verbose: bool = False) -> str:
     host_obj = os.path.join(BUILD_DIR, "psc_build.o")
     dev_obj = os.path.join(BUILD_DIR, "psc_device.o")
     store_obj = os.path.join(BUILD_DIR, "psc_store.o")
+    gram_obj = os.path.join(BUILD_DIR, "psc_grammar.o")
     _run(["g++", *HOST_FLAGS, f"-I{ROCM}/include", "-c", os.path.join(CSRC, "psc_build.cpp"), "-o", host_obj])
     _run(["g++", *HOST_FLAGS, f"-I{ROCM}/include", "-c", os.path.join(CSRC, "psc_store.cpp"), "-o", store_obj])
+    _run(["g++", *HOST_FLAGS, f"-I{ROCM}/include", "-c", os.path.join(CSRC, "psc_grammar.cpp"), "-o", gram_obj])
     _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, "psc_device.hip"), "-o", dev_obj])
     tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", host_obj, store_obj, dev_obj, "-lz", "-o", tmp])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", host_obj, store_obj, gram_obj, dev_obj, "-lz", "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libpsc.so")
 
 PSC_F32, PSC_BF16 = 0, 1
 ADV_OK, ADV_REJECTED, ADV_EOS, ADV_OVERFLOW, ADV_BAD_INPUT, ADV_SKIPPED = range(6)
-_STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -4: "PSC_E_OOM",
+_STATUS = {0: "PSC_OK", -1: "PSC_E_INVALID_ARG", -2: "PSC_E_GRAMMAR", -3: "PSC_E_NOT_LALR1", -4: "PSC_E_OOM",
            -5: "PSC_E_DEVICE", -6: "PSC_E_NOT_BOUND", -7: "PSC_E_LIMIT", -8: "PSC_E_IO", -9: "PSC_E_FORMAT",
            -10: "PSC_E_NOT_VIABLE"}
 
@@ -28,7 +28,8 @@ EXPORTED = ["psc_build", "psc_info", "psc_device_bytes", "psc_bind_device", "psc
             "psc_host_state", "psc_free", "psc_last_error", "psc_device_bytes_ex", "psc_bind_device_ex",
             "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n", "psc_compute_and_argmax_n",
             "psc_predictor_fill", "psc_predictor_updates", "psc_timeline_records", "psc_compute_and_apply_timeline",
-            "psc_set_options", "psc_compute_and_argmax_noalloc"]
+            "psc_set_options", "psc_compute_and_argmax_noalloc", "psc_grammar_compile", "psc_grammar_view",
+            "psc_grammar_symbol_name", "psc_grammar_free", "psc_build_from_text"]
 
 BIND_FLAT, BIND_SLICED = 1, 2
 OPT_SPECULATE = 1
@@ -196,6 +197,13 @@ def lib() -> C.CDLL:
         L.psc_compute_and_apply_n.argtypes = [P, P, I64, P, P, I32, P, P, C.c_int, I32, P]
         L.psc_compute_and_argmax_n.argtypes = [P, P, I64, P, P, I32, P, C.c_int, I32, P, P]
         L.psc_compute_and_argmax_noalloc.argtypes = [P, P, I64, P, P, I32, P, C.c_int, I32, P, P]
+        L.psc_grammar_compile.argtypes = [C.c_char_p, C.c_size_t, C.POINTER(P)]
+        L.psc_grammar_view.argtypes = [P, P]
+        L.psc_grammar_symbol_name.argtypes = [P, I32, I32]
+        L.psc_grammar_symbol_name.restype = C.c_char_p
+        L.psc_grammar_free.argtypes = [P]
+        L.psc_grammar_free.restype = None
+        L.psc_build_from_text.argtypes = [C.c_char_p, C.c_size_t, P, C.POINTER(P)]
         L.psc_predictor_fill.argtypes = [P, I32, P]
         L.psc_set_options.argtypes = [P, C.c_uint32]
         L.psc_predictor_updates.argtypes = [P, P, I32, P]
@@ -212,7 +220,8 @@ def lib() -> C.CDLL:
                      "psc_classify_host", "psc_class_mask_host", "psc_host_state", "psc_bind_device_ex",
                      "psc_compute_masks_n", "psc_compute_classes_n", "psc_compute_and_apply_n",
                      "psc_compute_and_argmax_n", "psc_predictor_fill", "psc_predictor_updates",
-                     "psc_compute_and_apply_timeline", "psc_set_options", "psc_compute_and_argmax_noalloc"):
+                     "psc_compute_and_apply_timeline", "psc_set_options", "psc_compute_and_argmax_noalloc",
+                     "psc_grammar_compile", "psc_grammar_view", "psc_build_from_text"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -244,9 +253,64 @@ def pack_states(states, device=None):
     return t(stacks if stacks.size else np.zeros(1, np.int32)), t(lens), t(qs)
 
 
+class CompiledGrammar:
+    """Grammar text compiled by the library (psc_grammar_compile): the lexer
+    and LALR(1) tables psc_build takes, as numpy arrays, with the symbol
+    names.  Raises PscError (PSC_E_NOT_LALR1 on a conflict)."""
+
+    def __init__(self, text):
+        data = text.encode("latin-1") if isinstance(text, str) else bytes(text)
+        h = C.c_void_p()
+        _check(lib().psc_grammar_compile(data, len(data), C.byref(h)))
+        try:
+            v = _Grammar()
+            _check(lib().psc_grammar_view(h, C.addressof(v)))
+
+            def arr(ptr, n, ct, dt):
+                return np.ctypeslib.as_array(C.cast(ptr, C.POINTER(ct)), shape=(n,)).astype(dt).copy() \
+                    if n else np.zeros(0, dt)
+            nq, nt, ns, nn, npr = v.n_lex_states, v.n_terminals, v.n_lr_states, v.n_nonterminals, v.n_productions
+            self.lex_next = arr(v.lex_next, nq * 256, C.c_int32, np.int32).reshape(nq, 256)
+            self.lex_accept = arr(v.lex_accept, nq, C.c_int32, np.int32)
+            self.terminal_ignored = arr(v.terminal_ignored, nt, C.c_uint8, np.uint8)
+            self.end_terminal = int(v.end_terminal)
+            self.action = arr(v.action, ns * nt, C.c_int32, np.int32).reshape(ns, nt)
+            self.goto = arr(v.goto_table, ns * nn, C.c_int32, np.int32).reshape(ns, nn)
+            self.prod_lhs = arr(v.prod_lhs, npr, C.c_int32, np.int32)
+            self.prod_len = arr(v.prod_len, npr, C.c_int32, np.int32)
+            name = lambda term, i: lib().psc_grammar_symbol_name(h, term, i).decode("latin-1")
+            self.terminal_names = [name(1, i) for i in range(nt)]
+            self.nonterminal_names = [name(0, i) for i in range(nn)]
+        finally:
+            lib().psc_grammar_free(h)
+
+
+def _vocab_struct(vocab):
+    toks = vocab.tokens
+    offs = np.zeros(len(toks) + 1, dtype=np.int64)
+    np.cumsum([len(t) for t in toks], out=offs[1:])
+    blob = np.frombuffer(b"".join(toks) + b"\0", dtype=np.uint8).copy()
+    return _Vocab(len(toks), blob.ctypes.data, offs.ctypes.data, int(vocab.eos_id)), (blob, offs)
+
+
 class Classifier:
-    """A built (grammar, vocabulary) classifier: psc_build .. psc_free; or one
-    read back with Classifier.load(path)."""
+    """A built (grammar, vocabulary) classifier: psc_build .. psc_free; one
+    built from grammar text with Classifier.from_text; or one read back with
+    Classifier.load(path)."""
+
+    @classmethod
+    def from_text(cls, text, vocab) -> "Classifier":
+        """psc_build_from_text: compile the grammar text, then build."""
+        data = text.encode("latin-1") if isinstance(text, str) else bytes(text)
+        vs, keep = _vocab_struct(vocab)
+        h = C.c_void_p()
+        _check(lib().psc_build_from_text(data, len(data), C.addressof(vs), C.byref(h)))
+        self = cls.__new__(cls)
+        self._h = h
+        self._dev = None
+        self.V = len(vocab.tokens)
+        self.W = (self.V + 31) // 32
+        return self
 
     @classmethod
     def load(cls, path: str) -> "Classifier":

@@ -20,7 +20,7 @@ from oracle import Oracle
 CHARS = ["a", "b", "c", "(", ")", ","]
 
 
-def _random_grammar(rng):
+def _random_grammar(rng, compiled=True):
     n_nt = int(rng.integers(2, 6))
     nts = [f"n{i}" for i in range(n_nt)]
     g = Grammar("n0")
@@ -37,7 +37,7 @@ def _random_grammar(rng):
         if i + 1 < n_nt:                          # the next nonterminal is reachable, nested
             alts.add('"(" %s ")"' % nts[i + 1] if rng.random() < 0.5 else "%s %s" % (nts[i + 1], rng.choice(terms)))
         g.rule(nt, *sorted(alts))
-    return g.compile()
+    return g.compile() if compiled else g
 
 
 def _random_vocab(rng):

@@ -1,12 +1,13 @@
 """The host side of the library under AddressSanitizer + UndefinedBehaviour-
 Sanitizer, and the construction's thread pool under ThreadSanitizer.
 
-The construction and persistence sources are built with g++ and a sanitizer
+The construction, persistence and grammar-text sources are built with g++ and a sanitizer
 into a temporary shared library (no device code: the calls exercised are
 the construction, the host walk, the class rows, saving and loading), which
 a child Python process loads with the sanitizer runtime preloaded.  The
-child builds the small workloads, random grammars and a keyword grammar with
-dense rows and thousands of lexer states, compares the host walk
+child compiles the grammars from their text and some malformed ones, builds
+the small workloads, random grammars and a keyword grammar with dense rows
+and thousands of lexer states, compares the host walk
 with the oracle, round-trips the classifier through a file, and loads
 damaged files.  Any sanitizer report ends the child with an error.
 """
@@ -37,6 +38,14 @@ L.psc_device_bytes.restype = C.c_size_t
 L.psc_free.argtypes = [P]
 L.psc_free.restype = None
 L.psc_last_error.restype = C.c_char_p
+L.psc_grammar_compile.argtypes = [C.c_char_p, C.c_size_t, C.POINTER(P)]
+L.psc_grammar_compile.restype = C.c_int
+L.psc_grammar_view.argtypes = [P, P]
+L.psc_grammar_view.restype = C.c_int
+L.psc_grammar_symbol_name.argtypes = [P, I32, I32]
+L.psc_grammar_symbol_name.restype = C.c_char_p
+L.psc_grammar_free.argtypes = [P]
+L.psc_grammar_free.restype = None
 psc._lib = L                       # host calls only: nothing here binds a device
 from inputs import configs
 from oracle import Oracle
@@ -52,6 +61,17 @@ if sys.argv[7] == "1":                 # dense rows, and more lexer states than 
 for seed, g, vocab, rng in RG._cases(int(sys.argv[6])):
     orc = Oracle(g, vocab)
     cases.append((f"random{seed}", g, vocab, RG._walk_states(orc, vocab, rng, n_walks=3, n_tokens=12)))
+for name, g, vocab, states in cases:          # the grammar text front end
+    if getattr(g, "text", ""):
+        c = psc.CompiledGrammar(g.text)
+        assert np.array_equal(c.action, g.action) and np.array_equal(c.lex_next, g.lexer.next), name
+for bad in ['%start e\nN: /[0-9]/\ne: e "+" e | N\n', '%start s\nA: /(a/\ns: A\n', '%start s\ns: "a\n',
+            '%start s\nA: /a{3,1}/\ns: A\n', '%start s\nA: /[b-a]/\ns: A\n', '%start s\nA: /a\\x4/\ns: A\n']:
+    try:
+        psc.CompiledGrammar(bad)
+        raise SystemExit("accepted " + bad)
+    except psc.PscError:
+        pass
 for name, g, vocab, states in cases:
     clf = psc.Classifier(g, vocab)
     want = Oracle(g, vocab).masks(states)
@@ -77,7 +97,7 @@ def _build(tmp_path, flags):
     subprocess.check_call(["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fPIC", "-shared",
                            *flags, f"-I{os.environ.get('ROCM_PATH', '/opt/rocm')}/include",
                            os.path.join(CSRC, "psc_build.cpp"), os.path.join(CSRC, "psc_store.cpp"),
-                           "-lz", "-o", so])
+                           os.path.join(CSRC, "psc_grammar.cpp"), "-lz", "-o", so])
     return so
 
 
