@@ -62,6 +62,11 @@ struct CompileError {
 
 [[noreturn]] void fail(psc_status code, const std::string &msg) { throw CompileError{code, msg}; }
 
+// Bounds that keep hostile text from exhausting the stack or memory.
+constexpr int kMaxRegexDepth = 500;        // nested groups in one regex
+constexpr size_t kMaxNfaStates = 4000000;  // all terminals together
+constexpr size_t kMaxDfaStates = 1000000;  // before minimisation
+
 // ---------------------------------------------------------------- byte sets
 
 struct ByteSet {
@@ -135,6 +140,7 @@ class RegexParser {
     const std::string &p_;
     std::vector<Node> &nodes_;
     size_t i_ = 0;
+    int depth_ = 0;
 
     [[noreturn]] void bad(const std::string &m) const { fail(PSC_E_GRAMMAR, "regex /" + p_ + "/: " + m); }
     int peek() const { return i_ < p_.size() ? (unsigned char)p_[i_] : -1; }
@@ -189,7 +195,8 @@ class RegexParser {
 
     int repeat() {
         int node = atom();
-        for (;;) {
+        for (int ops = 0;; ops++) {
+            if (ops > kMaxRegexDepth) bad("more than " + std::to_string(kMaxRegexDepth) + " repetition operators in a row");
             const int c = peek();
             if (c == '*' || c == '+' || c == '?') {
                 take();
@@ -255,7 +262,9 @@ class RegexParser {
         const int c = take();
         if (c == '(') {
             if (p_.compare(i_, 2, "?:") == 0) i_ += 2;
+            if (++depth_ > kMaxRegexDepth) bad("groups nested deeper than " + std::to_string(kMaxRegexDepth));
             const int n = alt();
+            depth_--;
             if (peek() != ')') bad("missing )");
             take();
             return n;
@@ -317,6 +326,8 @@ struct Nfa {
     std::vector<int> accept;   // terminal id per state, -1
 
     int make() {
+        if (eps.size() >= kMaxNfaStates)
+            fail(PSC_E_LIMIT, "the terminals' NFA exceeds " + std::to_string(kMaxNfaStates) + " states");
         eps.emplace_back();
         edges.emplace_back();
         accept.push_back(-1);
@@ -502,6 +513,8 @@ Lexer build_lexer(const std::vector<Terminal> &terms, const std::vector<Node> &n
                 j = (int)order.size();
                 ids.emplace(tgt, j);
                 order.push_back(std::move(tgt));
+                if (order.size() > kMaxDfaStates)
+                    fail(PSC_E_LIMIT, "the lexer DFA exceeds " + std::to_string(kMaxDfaStates) + " states");
             } else {
                 j = it->second;
             }

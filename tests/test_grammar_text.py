@@ -114,6 +114,10 @@ expr: expr "+" NUM | NUM | ID | "\"s\""
     ('%start s\n%bogus\ns: "a"\n', -2, "unknown directive"),
     ('%start t\ns: "a"\n', -2, "start symbol t has no rules"),
     ('', -2, "no %start"),
+    ('%start s\nA: /' + '(' * 600 + 'a' + ')' * 600 + '/\ns: A\n', -2, "nested deeper than 500"),
+    ('%start s\nA: /a' + '*' * 600 + '/\ns: A\n', -2, "repetition operators in a row"),
+    ('%start s\nA: /((((a{100}){100}){100}){100})/\ns: A\n', -7, "NFA exceeds"),
+    ('%start s\nA: /[ab]*a[ab]{21}/\ns: A\n', -7, "lexer DFA exceeds"),
 ])
 def test_errors_are_reported(text, status, needle):
     with pytest.raises(PscError) as e:
