@@ -1043,14 +1043,9 @@ void start_blocks(const psc_handle &h, std::vector<int32_t> &out) {
         if (ref < 0 || (ref & 3) == kRefDense) continue;
         const int64_t row = ref & ~3;
         int32_t *blk = out.data() + (size_t)q * kStartBlockInts;
-        for (int lane = 0; lane < 64; lane++) {
-            if ((ref & 3) == kRefChain) {
-                for (int k = 0; k < kChainEntry; k++) blk[4 * lane + k] = at(row + kChainEntry * lane + k);
-            } else {
-                blk[4 * lane] = at(row + 2 * lane);
-                blk[4 * lane + 1] = at(row + 2 * lane + 1);
-            }
-        }
+        // chain entries and sparse rows are both 16 bytes per lane
+        for (int lane = 0; lane < 64; lane++)
+            for (int k = 0; k < 4; k++) blk[4 * lane + k] = at(row + 4 * lane + k);
     }
 }
 }  // namespace psc
@@ -1323,7 +1318,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             bool is_dense = ne > kSparseMax;
             ref[b] = (int32_t)off | (is_dense ? kRefDense : 0);
-            int64_t len = kRowHeader + (is_dense ? (int64_t)G.nPi : 2LL * ne);
+            int64_t len = is_dense ? kRowHeader + (int64_t)G.nPi : kSparseHeader + (int64_t)kSparseEdge * ne;
             off += (len + 3) & ~3;
             if (is_dense) dense++; else max_sparse = std::max(max_sparse, ne);
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
@@ -1344,17 +1339,25 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             int32_t *row = h->table.data() + ref_offset(ref[b]);
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             row[0] = m_cls[b];
-            row[2] = ref[m_def[b]];
-            row[3] = 0;
             if (ref_is_dense(ref[b])) {
                 row[1] = -1;
+                row[2] = ref[m_def[b]];
+                row[3] = 0;
                 for (int32_t X = 0; X < G.nPi; X++) row[kRowHeader + X] = ref[m_def[b]];
                 for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) row[kRowHeader + m_sym[e]] = ref[m_tgt[e]];
             } else {
                 row[1] = ne;
+                row[2] = row[3] = 0;
+                row[4] = kSymNone;
+                row[5] = ref[m_def[b]];
+                row[6] = kNoSkip;   // set below, once the chains are laid out
+                row[7] = 0;
                 for (int32_t e = 0; e < ne; e++) {
-                    row[kRowHeader + 2 * e] = m_sym[m_ebeg[b] + e];
-                    row[kRowHeader + 2 * e + 1] = ref[m_tgt[m_ebeg[b] + e]];
+                    int32_t *en = row + kSparseHeader + kSparseEdge * e;
+                    en[0] = m_sym[m_ebeg[b] + e];
+                    en[1] = ref[m_tgt[m_ebeg[b] + e]];
+                    en[2] = kNoSkip;
+                    en[3] = 0;
                 }
             }
         }
@@ -1376,6 +1379,20 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             e[1] = 0;
             e[2] = ref[jump_to[c]];
             e[3] = 0;
+        }
+        // the skips of the sparse rows' refs (default and edges)
+        {
+            const int32_t *t = h->table.data();
+            const int64_t n = (int64_t)h->table.size();
+            for (int32_t b : order) {
+                if (det[b] >= 0 || is_thin(b) || ref_is_dense(ref[b])) continue;
+                int32_t *row = h->table.data() + ref_offset(ref[b]);
+                row[6] = chain_skip(t, n, row[5]);
+                for (int32_t e = 0; e < row[1]; e++) {
+                    int32_t *en = row + kSparseHeader + kSparseEdge * e;
+                    en[2] = chain_skip(t, n, en[1]);
+                }
+            }
         }
         h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);
         for (int32_t c = 0; c < h->n_classes; c++)
@@ -1468,13 +1485,25 @@ extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stac
             if (ref_is_dense(ref)) {
                 ref = row[kRowHeader + X];
             } else {
-                int32_t lo = 0, hi = row[1], nxt = row[2];
+                int32_t lo = 0, hi = row[1], nxt = row[5], skip = row[6];
                 while (lo < hi) {
-                    int32_t mid = (lo + hi) / 2, s = row[kRowHeader + 2 * mid];
-                    if (s == X) { nxt = row[kRowHeader + 2 * mid + 1]; break; }
-                    if (s < X) lo = mid + 1; else hi = mid;
+                    const int32_t mid = (lo + hi) / 2;
+                    const int32_t *en = row + kSparseHeader + kSparseEdge * mid;
+                    if (en[0] == X) { nxt = en[1]; skip = en[2]; break; }
+                    if (en[0] < X) lo = mid + 1; else hi = mid;
                 }
                 ref = nxt;
+                // a skip reads its k symbols (in range) without visiting the
+                // wildcard entries, as the device walk does
+                if (skip != kNoSkip) {
+                    const int32_t k = (int32_t)((uint32_t)skip >> 27);
+                    bool ok = i - (k - 1) >= 0;
+                    for (int32_t j = 0; ok && j < k; j++) ok = st[i - j] >= 0 && st[i - j] < h->n_lr;
+                    if (ok) {
+                        i -= k;
+                        ref = (int32_t)(((uint32_t)skip & ((1u << 27) - 1)) - (1u << 26));
+                    }
+                }
             }
         }
         out_classes[b] = cls;

@@ -172,23 +172,42 @@ struct Walk {
         return false;
     }
 
-    // One step from a sparse row (lane 0: end_class, n_edges; lane 1:
-    // default; lane j >= 2: edge j-2).
-    __device__ __forceinline__ bool row_step(const int2 v, int X) {
-        const int va = v.x, vc = v.y;
-        if (i < 0) { cls = __builtin_amdgcn_readlane(va, 0); return true; }
-        const int n = __builtin_amdgcn_readlane(vc, 0);
-        const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && va == X);
-        const int nref = hit ? __builtin_amdgcn_readlane(vc, __ffsll((long long)hit) - 1)
-                             : __builtin_amdgcn_readlane(va, 1);
+    // One step from a sparse row, 16 bytes per lane: lane 0 (end_class,
+    // n_edges), lane 1 (-, default, default's skip), lane j >= 2 edge j - 2
+    // (symbol, ref, skip); the edge matching the symbol is found with a
+    // ballot and read with readlane.  A skip of k wildcard entries then reads
+    // the next k symbols from the window without a load (only their range is
+    // checked) and goes on at the chain's jump target, as the chain would;
+    // when the stack ends within them, they reach past the window, or one is
+    // out of range, the walk takes the chain itself.
+    __device__ __forceinline__ bool row_step(const int4 v, int X) {
+        if (i < 0) { cls = __builtin_amdgcn_readlane(v.x, 0); return true; }
+        const int n = __builtin_amdgcn_readlane(v.y, 0);
+        const unsigned long long hit = __ballot(lane >= 2 && lane - 2 < n && v.x == X);
+        const int h = hit ? __ffsll((long long)hit) - 1 : 1;
+        const int nref = __builtin_amdgcn_readlane(v.y, h);
+        const int nskip = __builtin_amdgcn_readlane(v.z, h);
         if (kTrack) {
-            exit_lane = hit ? __ffsll((long long)hit) - 1 : 1;
+            exit_lane = h;
             exit_kind = 0;
         }
         // a symbol out of range ends the walk through kRefFault; a select,
         // not a branch, so that the row load cannot sink below the window
-        ref = X >= 0 && X < n_lr ? nref : kRefFault;
+        const bool ok = X >= 0 && X < n_lr;
+        ref = ok ? nref : kRefFault;
         i--;
+        if (ok && nskip != kNoSkip) {
+            const int k = (int)((uint32_t)nskip >> 27);
+            const int lo = chunk_base - i;          // window lane of stack index i
+            const unsigned long long valid = __ballot(sym >= 0 && sym < n_lr);
+            if (i - (k - 1) >= 0 && lo + k <= kChunk) {
+                const unsigned long long need = ((1ull << k) - 1) << lo;
+                if ((valid & need) == need) {
+                    i -= k;
+                    ref = (int)(((uint32_t)nskip & ((1u << 27) - 1)) - (1u << 26));
+                }
+            }
+        }
         return false;
     }
 
@@ -198,7 +217,7 @@ struct Walk {
         if ((ref & 3) == kRefChain) return chain_step(blk);
         if ((ref & 3) == kRefDense) return step();
         const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
-        return row_step(make_int2(blk.x, blk.y), X);
+        return row_step(blk, X);
     }
 
     // One step: the one table load, then its evaluation.  A chain or sparse
@@ -216,7 +235,7 @@ struct Walk {
             i--;
             return false;
         }
-        const int2 v = *reinterpret_cast<const int2 *>(row + 2 * lane);
+        const int4 v = *reinterpret_cast<const int4 *>(row + kSparseEdge * lane);
         const int X = i >= 0 ? __builtin_amdgcn_readlane(sym, chunk_base - i) : 0;
         return row_step(v, X);
     }
@@ -245,8 +264,7 @@ __device__ __forceinline__ int walk_class(const int32_t *__restrict__ table, int
     if (q >= nb) {
         // no start block: the same load from the row itself
         const int32_t *row = table + (w.ref & ~3);
-        if ((w.ref & 3) == kRefChain) bv = *reinterpret_cast<const u32x4 *>(row + kChainEntry * lane);
-        else if ((w.ref & 3) != kRefDense) bv.xy = *reinterpret_cast<const u32x2 *>(row + 2 * lane);
+        if ((w.ref & 3) != kRefDense) bv = *reinterpret_cast<const u32x4 *>(row + 4 * lane);
     }
     if (w.first_step(make_int4((int)bv[0], (int)bv[1], (int)bv[2], (int)bv[3]))) return w.cls;
     for (;;) {
@@ -299,8 +317,7 @@ struct WalkRun {
         const bool has_block = q < nb;
         if (!has_block) {
             const int32_t *row = table + (w.ref & ~3);
-            if ((w.ref & 3) == kRefChain) bv = *reinterpret_cast<const u32x4 *>(row + kChainEntry * lane);
-            else if ((w.ref & 3) != kRefDense) bv.xy = *reinterpret_cast<const u32x2 *>(row + 2 * lane);
+            if ((w.ref & 3) != kRefDense) bv = *reinterpret_cast<const u32x4 *>(row + 4 * lane);
         }
         const bool dense = (w.ref & 3) == kRefDense;
         if (w.first_step(make_int4((int)bv[0], (int)bv[1], (int)bv[2], (int)bv[3]))) {

@@ -16,10 +16,14 @@ namespace psc {
 //              0 sparse row, 1 dense row, 2 chain entry.
 //   ref <  0 : the state is determined -- every stack continuation ends in
 //              the same class -- and that class is (-ref - 1).
-// Sparse and dense rows have a 4-int32 header: end_class, n_edges (sparse)
-// or -1 (dense), default_ref, 0.  Sparse rows follow with n_edges pairs
-// (symbol, ref) sorted by symbol; dense rows with n_lr_states refs indexed
-// by symbol.
+// Dense rows have a 4-int32 header (end_class, -1, default_ref, 0) and then
+// n_lr_states refs indexed by symbol.  Sparse rows are 16 bytes per lane of
+// one wavefront-wide load: (end_class, n_edges, 0, 0), (kSymNone,
+// default_ref, default_skip, 0), then n_edges entries (symbol, ref, skip, 0)
+// sorted by symbol.  A skip (chain_skip) is set when the ref is a chain entry
+// from which k >= 1 wildcard entries lead to the chain's jump: the walk may
+// then read those k symbols without a load (checking only that they are in
+// range) and go on at the jump's target, as the chain would.
 //
 // Chains: a state with at most two explicit edges (an edge-free state
 // included) is one 16-byte entry of a chain, so that a walk through a run
@@ -37,7 +41,9 @@ namespace psc {
 // copies of the thin states its last state continues into (their entries,
 // never pointed at by a ref), up to kChainReach entries in all.
 // Rows and entries start at multiples of 4 int32 (16-byte aligned).
-constexpr int kRowHeader = 4;
+constexpr int kRowHeader = 4;       // dense rows
+constexpr int kSparseHeader = 8;    // sparse rows: two 16-byte header entries
+constexpr int kSparseEdge = 4;      // int32 per sparse entry
 constexpr int kSparseMax = 62;      // header + edges in one wavefront-wide load
 constexpr int kChainMax = 63;
 constexpr int kChainReach = 16;     // entries a chain is extended to with copies of its continuation
@@ -48,12 +54,33 @@ constexpr int kRefDense = 1, kRefChain = 2;
 // a walk step reads 64 lanes x 16 bytes from a chain entry speculatively
 constexpr int kTablePad = 64 * kChainEntry + kRowHeader;
 
+// A skip: k (1..kSkipMax) wildcard entries, then the jump's target ref R,
+// packed as k << 27 | (R + 2^26); kNoSkip when there is none or R does not fit.
+constexpr int32_t kNoSkip = -1;
+constexpr int kSkipMax = 15;
+inline int32_t skip_encode(int k, int32_t target) {
+    if (k < 1 || k > kSkipMax || target < -(1 << 26) || target >= (1 << 26)) return kNoSkip;
+    return (int32_t)(((uint32_t)k << 27) | (uint32_t)(target + (1 << 26)));
+}
+
 inline bool ref_is_class(int32_t ref) { return ref < 0; }
 inline int32_t ref_class(int32_t ref) { return -ref - 1; }
 inline int32_t class_ref(int32_t cls) { return -cls - 1; }
 inline bool ref_is_dense(int32_t ref) { return (ref & 3) == kRefDense; }
 inline bool ref_is_chain(int32_t ref) { return (ref & 3) == kRefChain; }
 inline int32_t ref_offset(int32_t ref) { return ref & ~3; }
+
+// The skip of `ref` in a table of n int32 (kNoSkip unless ref is a chain
+// entry followed, from itself, by 1..kSkipMax wildcard entries and the jump).
+inline int32_t chain_skip(const int32_t *t, int64_t n, int32_t ref) {
+    if (ref < 0 || !ref_is_chain(ref)) return kNoSkip;
+    const int64_t p = ref_offset(ref);
+    int k = 0;
+    while (k <= kSkipMax && p + kChainEntry * k < n && (t[p + kChainEntry * k] & 0xFFFF) == kSymWild) k++;
+    const int64_t j = p + kChainEntry * k;
+    if (k < 1 || k > kSkipMax || j + 2 >= n || (t[j] & 0xFFFF) != kSymJump) return kNoSkip;
+    return skip_encode(k, t[j + 2]);
+}
 
 // The problem instance as the device advance of prefix states reads it: one
 // int32 blob, sections at these int32 offsets, plus the vocabulary bytes.
@@ -75,8 +102,8 @@ struct AdvanceLayout {
 //                              faults), [1] updates of the class predictor (+ padding)
 //   [256, table_off(n_lex))    start blocks [min(n_lex, kMaxStartBlocks)][64 lanes][4] int32: block q holds the
 //                              first walk step's wavefront load from start[q] (the 64
-//                              chain entries, or the sparse row's pairs in .x/.y), so that
-//                              it is fetched together with the stack instead of after it
+//                              chain entries, or the sparse row's header and entries), so
+//                              that it is fetched together with the stack instead of after it
 //   [table_off(n_lex), ...)    int32 table: start refs [n_lex], rows, pad
 //   [mask_off, ...)            flat layout: uint32 masks [n_classes][mask_stride] (256-B aligned);
 //                              sliced layout: uint32 slices [n_unique_slices][64], then
@@ -157,7 +184,7 @@ size_t goto_closure_bytes(const psc_handle &h);
 void goto_closure(const psc_handle &h, std::vector<int32_t> &out);
 // The start blocks, [start_block_count(n_lex)][kStartBlockInts]: block q is what a walk's
 // first step from start[q] loads, one 16-byte vector per lane (a chain
-// entry's 64 entries as they are; a sparse row's int32 pairs in .x/.y);
+// entry's 64 entries, or a sparse row's header and entries, as they are);
 // zeros for a determined start or a dense row, which the walk does not read.
 void start_blocks(const psc_handle &h, std::vector<int32_t> &out);
 // The input checks of psc_build (ids in range, spellings), for loaded tables.

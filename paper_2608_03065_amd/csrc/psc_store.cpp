@@ -31,7 +31,7 @@ using namespace psc;
 namespace {
 
 constexpr char kMagic[4] = {'P', 'S', 'C', 'B'};
-constexpr uint32_t kVersion = 1;
+constexpr uint32_t kVersion = 2;   // 2: 16-byte sparse entries with skips
 constexpr uint32_t kCodecRaw = 0, kCodecZlib = 1;
 constexpr uint64_t kMaxSection = 1ull << 40;      // sanity bound on a section's size
 constexpr size_t kCompressAbove = 1 << 16;        // smaller sections are stored raw
@@ -152,7 +152,7 @@ void check_loaded(const psc_handle &h) {
             len = kRowHeader + h.n_lr;
         } else if (n >= 0 && n <= kSparseMax) {
             kind[pos / 4] = 1;
-            len = kRowHeader + 2 * (int64_t)n;
+            len = kSparseHeader + kSparseEdge * (int64_t)n;
         } else {
             bad("row header");
         }
@@ -184,16 +184,18 @@ void check_loaded(const psc_handle &h) {
         if (!ref_ok(t[q])) bad("start ref");
     for (int64_t pos = h.rows_off; pos < h.chains_off;) {
         const int32_t *row = t + pos;
-        if (!cls_ok(row[0]) || !ref_ok(row[2])) bad("row header refs");
+        if (!cls_ok(row[0])) bad("row end class");
         int64_t len = 0;
         if (row[1] == -1) {
+            if (!ref_ok(row[2])) bad("dense row default");
             for (int32_t x = 0; x < h.n_lr; x++)
                 if (!ref_ok(row[kRowHeader + x])) bad("dense row ref");
             len = kRowHeader + h.n_lr;
         } else {
+            if (row[4] != kSymNone || !ref_ok(row[5])) bad("sparse row default");
             for (int32_t e = 0; e < row[1]; e++)
-                if (!ref_ok(row[kRowHeader + 2 * e + 1])) bad("sparse row ref");
-            len = kRowHeader + 2 * (int64_t)row[1];
+                if (!ref_ok(row[kSparseHeader + kSparseEdge * e + 1])) bad("sparse row ref");
+            len = kSparseHeader + kSparseEdge * (int64_t)row[1];
         }
         pos += (len + 3) & ~3;
     }
@@ -205,6 +207,21 @@ void check_loaded(const psc_handle &h) {
             continue;
         }
         if (!cls_ok(e[3]) || !ref_ok(e[2]) || ((x >> 16) != kSymNone && !ref_ok(e[1]))) bad("chain entry refs");
+    }
+    // every skip is the one its ref's chain gives (so its target is a
+    // validated jump ref)
+    for (int64_t pos = h.rows_off; pos < h.chains_off;) {
+        const int32_t *row = t + pos;
+        int64_t len = kRowHeader + h.n_lr;
+        if (row[1] != -1) {
+            if (row[6] != chain_skip(t, T, row[5])) bad("sparse row default skip");
+            for (int32_t e = 0; e < row[1]; e++) {
+                const int32_t *en = row + kSparseHeader + kSparseEdge * e;
+                if (en[2] != chain_skip(t, T, en[1])) bad("sparse row skip");
+            }
+            len = kSparseHeader + kSparseEdge * (int64_t)row[1];
+        }
+        pos += (len + 3) & ~3;
     }
     // tail bits of every mask row are zero
     const uint32_t tail = h.V % 32 ? ~0u << (h.V % 32) : 0u;
