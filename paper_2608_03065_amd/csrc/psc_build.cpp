@@ -1318,7 +1318,7 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             int32_t ne = m_ebeg[b + 1] - m_ebeg[b];
             bool is_dense = ne > kSparseMax;
             ref[b] = (int32_t)off | (is_dense ? kRefDense : 0);
-            int64_t len = is_dense ? kRowHeader + (int64_t)G.nPi : kSparseHeader + (int64_t)kSparseEdge * ne;
+            int64_t len = is_dense ? kRowHeader + 2LL * G.nPi : kSparseHeader + (int64_t)kSparseEdge * ne;
             off += (len + 3) & ~3;
             if (is_dense) dense++; else max_sparse = std::max(max_sparse, ne);
             if (off > (1LL << 30)) throw BuildError(PSC_E_LIMIT, "classifier table exceeds 4 GiB");
@@ -1343,8 +1343,11 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
                 row[1] = -1;
                 row[2] = ref[m_def[b]];
                 row[3] = 0;
-                for (int32_t X = 0; X < G.nPi; X++) row[kRowHeader + X] = ref[m_def[b]];
-                for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) row[kRowHeader + m_sym[e]] = ref[m_tgt[e]];
+                for (int32_t X = 0; X < G.nPi; X++) {
+                    row[kRowHeader + 2 * X] = ref[m_def[b]];
+                    row[kRowHeader + 2 * X + 1] = kNoSkip;   // set below
+                }
+                for (int32_t e = m_ebeg[b]; e < m_ebeg[b + 1]; e++) row[kRowHeader + 2 * m_sym[e]] = ref[m_tgt[e]];
             } else {
                 row[1] = ne;
                 row[2] = row[3] = 0;
@@ -1380,13 +1383,18 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
             e[2] = ref[jump_to[c]];
             e[3] = 0;
         }
-        // the skips of the sparse rows' refs (default and edges)
+        // the skips of the rows' refs (sparse defaults and edges, dense entries)
         {
             const int32_t *t = h->table.data();
             const int64_t n = (int64_t)h->table.size();
             for (int32_t b : order) {
-                if (det[b] >= 0 || is_thin(b) || ref_is_dense(ref[b])) continue;
+                if (det[b] >= 0 || is_thin(b)) continue;
                 int32_t *row = h->table.data() + ref_offset(ref[b]);
+                if (ref_is_dense(ref[b])) {
+                    for (int32_t X = 0; X < G.nPi; X++)
+                        row[kRowHeader + 2 * X + 1] = chain_skip(t, n, row[kRowHeader + 2 * X]);
+                    continue;
+                }
                 row[6] = chain_skip(t, n, row[5]);
                 for (int32_t e = 0; e < row[1]; e++) {
                     int32_t *en = row + kSparseHeader + kSparseEdge * e;
@@ -1482,27 +1490,31 @@ extern "C" psc_status psc_classify_host(const psc_handle *h, const int32_t *stac
             if (i < 0) { cls = row[0]; break; }
             const int32_t X = st[i--];
             if (X < 0 || X >= h->n_lr) break;
+            int32_t nxt, skip;
             if (ref_is_dense(ref)) {
-                ref = row[kRowHeader + X];
+                nxt = row[kRowHeader + 2 * X];
+                skip = row[kRowHeader + 2 * X + 1];
             } else {
-                int32_t lo = 0, hi = row[1], nxt = row[5], skip = row[6];
+                int32_t lo = 0, hi = row[1];
+                nxt = row[5];
+                skip = row[6];
                 while (lo < hi) {
                     const int32_t mid = (lo + hi) / 2;
                     const int32_t *en = row + kSparseHeader + kSparseEdge * mid;
                     if (en[0] == X) { nxt = en[1]; skip = en[2]; break; }
                     if (en[0] < X) lo = mid + 1; else hi = mid;
                 }
-                ref = nxt;
-                // a skip reads its k symbols (in range) without visiting the
-                // wildcard entries, as the device walk does
-                if (skip != kNoSkip) {
-                    const int32_t k = (int32_t)((uint32_t)skip >> 27);
-                    bool ok = i - (k - 1) >= 0;
-                    for (int32_t j = 0; ok && j < k; j++) ok = st[i - j] >= 0 && st[i - j] < h->n_lr;
-                    if (ok) {
-                        i -= k;
-                        ref = (int32_t)(((uint32_t)skip & ((1u << 27) - 1)) - (1u << 26));
-                    }
+            }
+            ref = nxt;
+            // a skip reads its k symbols (in range) without visiting the
+            // wildcard entries, as the device walk does
+            if (skip != kNoSkip) {
+                const int32_t k = (int32_t)((uint32_t)skip >> 27);
+                bool ok = i - (k - 1) >= 0;
+                for (int32_t j = 0; ok && j < k; j++) ok = st[i - j] >= 0 && st[i - j] < h->n_lr;
+                if (ok) {
+                    i -= k;
+                    ref = (int32_t)(((uint32_t)skip & ((1u << 27) - 1)) - (1u << 26));
                 }
             }
         }

@@ -196,19 +196,24 @@ struct Walk {
         const bool ok = X >= 0 && X < n_lr;
         ref = ok ? nref : kRefFault;
         i--;
-        if (ok && nskip != kNoSkip) {
-            const int k = (int)((uint32_t)nskip >> 27);
-            const int lo = chunk_base - i;          // window lane of stack index i
-            const unsigned long long valid = __ballot(sym >= 0 && sym < n_lr);
-            if (i - (k - 1) >= 0 && lo + k <= kChunk) {
-                const unsigned long long need = ((1ull << k) - 1) << lo;
-                if ((valid & need) == need) {
-                    i -= k;
-                    ref = (int)(((uint32_t)nskip & ((1u << 27) - 1)) - (1u << 26));
-                }
+        if (ok) take_skip(nskip);
+        return false;
+    }
+
+    // After a row step: read the k wildcard symbols of `skip` from the window
+    // and go on at its target, when they are all there and in range.
+    __device__ __forceinline__ void take_skip(int skip) {
+        if (skip == kNoSkip) return;
+        const int k = (int)((uint32_t)skip >> 27);
+        const int lo = chunk_base - i;          // window lane of stack index i
+        const unsigned long long valid = __ballot(sym >= 0 && sym < n_lr);
+        if (i - (k - 1) >= 0 && lo + k <= kChunk) {
+            const unsigned long long need = ((1ull << k) - 1) << lo;
+            if ((valid & need) == need) {
+                i -= k;
+                ref = (int)(((uint32_t)skip & ((1u << 27) - 1)) - (1u << 26));
             }
         }
-        return false;
     }
 
     // The first step from start[q], whose wavefront load (the start block)
@@ -226,13 +231,14 @@ struct Walk {
         const int32_t *row = table + (ref & ~3);
         if ((ref & 3) == kRefChain) return chain_step(*reinterpret_cast<const int4 *>(row + kChainEntry * lane));
         if ((ref & 3) == kRefDense) {
-            // one uniform address: a scalar load
+            // one uniform address: a scalar load of the entry (ref, skip)
             if (i < 0) { cls = row[0]; return true; }
             const int X = __builtin_amdgcn_readlane(sym, chunk_base - i);
-            const int Xd = X >= 0 && X < n_lr ? X : 0;
-            const int nref = row[kRowHeader + Xd];
-            ref = X >= 0 && X < n_lr ? nref : kRefFault;
+            const bool ok = X >= 0 && X < n_lr;
+            const int2 e = *reinterpret_cast<const int2 *>(row + kRowHeader + 2 * (ok ? X : 0));
+            ref = ok ? e.x : kRefFault;
             i--;
+            if (ok) take_skip(e.y);
             return false;
         }
         const int4 v = *reinterpret_cast<const int4 *>(row + kSparseEdge * lane);

@@ -17,7 +17,7 @@ namespace psc {
 //   ref <  0 : the state is determined -- every stack continuation ends in
 //              the same class -- and that class is (-ref - 1).
 // Dense rows have a 4-int32 header (end_class, -1, default_ref, 0) and then
-// n_lr_states refs indexed by symbol.  Sparse rows are 16 bytes per lane of
+// n_lr_states entries (ref, skip) indexed by symbol.  Sparse rows are 16 bytes per lane of
 // one wavefront-wide load: (end_class, n_edges, 0, 0), (kSymNone,
 // default_ref, default_skip, 0), then n_edges entries (symbol, ref, skip, 0)
 // sorted by symbol.  A skip (chain_skip) is set when the ref is a chain entry

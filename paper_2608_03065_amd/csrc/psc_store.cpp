@@ -31,7 +31,7 @@ using namespace psc;
 namespace {
 
 constexpr char kMagic[4] = {'P', 'S', 'C', 'B'};
-constexpr uint32_t kVersion = 2;   // 2: 16-byte sparse entries with skips
+constexpr uint32_t kVersion = 3;   // 3: row entries carry skips
 constexpr uint32_t kCodecRaw = 0, kCodecZlib = 1;
 constexpr uint64_t kMaxSection = 1ull << 40;      // sanity bound on a section's size
 constexpr size_t kCompressAbove = 1 << 16;        // smaller sections are stored raw
@@ -149,7 +149,7 @@ void check_loaded(const psc_handle &h) {
         int64_t len = 0;
         if (n == -1) {
             kind[pos / 4] = 2;
-            len = kRowHeader + h.n_lr;
+            len = kRowHeader + 2 * (int64_t)h.n_lr;
         } else if (n >= 0 && n <= kSparseMax) {
             kind[pos / 4] = 1;
             len = kSparseHeader + kSparseEdge * (int64_t)n;
@@ -189,8 +189,8 @@ void check_loaded(const psc_handle &h) {
         if (row[1] == -1) {
             if (!ref_ok(row[2])) bad("dense row default");
             for (int32_t x = 0; x < h.n_lr; x++)
-                if (!ref_ok(row[kRowHeader + x])) bad("dense row ref");
-            len = kRowHeader + h.n_lr;
+                if (!ref_ok(row[kRowHeader + 2 * x])) bad("dense row ref");
+            len = kRowHeader + 2 * (int64_t)h.n_lr;
         } else {
             if (row[4] != kSymNone || !ref_ok(row[5])) bad("sparse row default");
             for (int32_t e = 0; e < row[1]; e++)
@@ -212,8 +212,11 @@ void check_loaded(const psc_handle &h) {
     // validated jump ref)
     for (int64_t pos = h.rows_off; pos < h.chains_off;) {
         const int32_t *row = t + pos;
-        int64_t len = kRowHeader + h.n_lr;
-        if (row[1] != -1) {
+        int64_t len = kRowHeader + 2 * (int64_t)h.n_lr;
+        if (row[1] == -1) {
+            for (int32_t x = 0; x < h.n_lr; x++)
+                if (row[kRowHeader + 2 * x + 1] != chain_skip(t, T, row[kRowHeader + 2 * x])) bad("dense row skip");
+        } else {
             if (row[6] != chain_skip(t, T, row[5])) bad("sparse row default skip");
             for (int32_t e = 0; e < row[1]; e++) {
                 const int32_t *en = row + kSparseHeader + kSparseEdge * e;
