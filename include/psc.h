@@ -121,6 +121,8 @@ typedef struct {
     int64_t sliced_mask_bytes; /* the mask table in the sliced layout: the
                                   distinct slices plus a slice id per row and
                                   slice (compare mask_table_bytes)            */
+    int64_t skip_edges;        /* row entries that carry a skip over a run of
+                                  wildcard chain states                       */
 } psc_info_t;
 
 /* Layouts of the mask table in the bound buffer (psc_bind_device_ex).

@@ -1387,20 +1387,26 @@ extern "C" psc_status psc_build(const psc_grammar *grammar, const psc_vocab *voc
         {
             const int32_t *t = h->table.data();
             const int64_t n = (int64_t)h->table.size();
+            int64_t skips = 0;
             for (int32_t b : order) {
                 if (det[b] >= 0 || is_thin(b)) continue;
                 int32_t *row = h->table.data() + ref_offset(ref[b]);
                 if (ref_is_dense(ref[b])) {
-                    for (int32_t X = 0; X < G.nPi; X++)
+                    for (int32_t X = 0; X < G.nPi; X++) {
                         row[kRowHeader + 2 * X + 1] = chain_skip(t, n, row[kRowHeader + 2 * X]);
+                        skips += row[kRowHeader + 2 * X + 1] != kNoSkip;
+                    }
                     continue;
                 }
                 row[6] = chain_skip(t, n, row[5]);
+                skips += row[6] != kNoSkip;
                 for (int32_t e = 0; e < row[1]; e++) {
                     int32_t *en = row + kSparseHeader + kSparseEdge * e;
                     en[2] = chain_skip(t, n, en[1]);
+                    skips += en[2] != kNoSkip;
                 }
             }
+            h->info.skip_edges = skips;
         }
         h->masks.assign((size_t)h->n_classes * h->mask_stride, 0);
         for (int32_t c = 0; c < h->n_classes; c++)

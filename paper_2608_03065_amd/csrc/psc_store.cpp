@@ -130,8 +130,9 @@ void read_section(FILE *f, uint32_t t, std::vector<T> &dst) {
     if (fnv1a(dst.data(), sh.raw_bytes) != sh.checksum) fail(PSC_E_FORMAT, "section checksum mismatch");
 }
 
-// Everything the device kernels rely on, checked on a loaded handle.
-void check_loaded(const psc_handle &h) {
+// Everything the device kernels rely on, checked on a loaded handle;
+// returns the number of skip edges.
+int64_t check_loaded(const psc_handle &h) {
     auto bad = [](const std::string &m) { fail(PSC_E_FORMAT, "invalid classifier: " + m); };
     if (h.V <= 0 || h.W != (h.V + 31) / 32 || h.mask_stride < h.W || h.mask_stride % 64 || h.n_lex <= 0 ||
         h.n_lr <= 0 || h.n_classes <= 0)
@@ -210,17 +211,22 @@ void check_loaded(const psc_handle &h) {
     }
     // every skip is the one its ref's chain gives (so its target is a
     // validated jump ref)
+    int64_t skips = 0;
     for (int64_t pos = h.rows_off; pos < h.chains_off;) {
         const int32_t *row = t + pos;
         int64_t len = kRowHeader + 2 * (int64_t)h.n_lr;
         if (row[1] == -1) {
-            for (int32_t x = 0; x < h.n_lr; x++)
+            for (int32_t x = 0; x < h.n_lr; x++) {
                 if (row[kRowHeader + 2 * x + 1] != chain_skip(t, T, row[kRowHeader + 2 * x])) bad("dense row skip");
+                skips += row[kRowHeader + 2 * x + 1] != kNoSkip;
+            }
         } else {
             if (row[6] != chain_skip(t, T, row[5])) bad("sparse row default skip");
+            skips += row[6] != kNoSkip;
             for (int32_t e = 0; e < row[1]; e++) {
                 const int32_t *en = row + kSparseHeader + kSparseEdge * e;
                 if (en[2] != chain_skip(t, T, en[1])) bad("sparse row skip");
+                skips += en[2] != kNoSkip;
             }
             len = kSparseHeader + kSparseEdge * (int64_t)row[1];
         }
@@ -260,6 +266,7 @@ void check_loaded(const psc_handle &h) {
     psc_vocab pv{h.V, h.vbytes.data(), offs.data(), L.eos};
     std::string msg;
     if (check_instance(&pg, &pv, &msg) != PSC_OK) bad(msg);
+    return skips;
 }
 
 }  // namespace
@@ -339,7 +346,7 @@ extern "C" psc_status psc_load(const char *path, psc_handle **out) {
         read_section(f.f, tag("MASK"), h->masks);
         read_section(f.f, tag("GRAM"), h->gram);
         read_section(f.f, tag("VBYT"), h->vbytes);
-        check_loaded(*h);
+        const int64_t skips = check_loaded(*h);
         // the sizes the statistics report are the validated ones
         h->info.vocab_size = h->V;
         h->info.mask_words = h->W;
@@ -349,6 +356,7 @@ extern "C" psc_status psc_load(const char *path, psc_handle **out) {
         h->info.n_classes = h->n_classes;
         h->info.table_bytes = (int64_t)h->table.size() * 4;
         h->info.mask_table_bytes = (int64_t)h->masks.size() * 4;
+        h->info.skip_edges = skips;
         slice_masks(*h);
         h->info.device_bytes = (int64_t)h->device_bytes_needed();
         *out = h.release();

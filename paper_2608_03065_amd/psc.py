@@ -148,6 +148,7 @@ class Info(C.Structure):
         ("mask_table_bytes", C.c_int64), ("device_bytes", C.c_int64), ("build_seconds", C.c_double),
         ("chain_states", C.c_int32), ("chains", C.c_int32), ("mask_slices_unique", C.c_int32),
         ("bound_mask_layout", C.c_int32), ("sliced_mask_bytes", C.c_int64),
+        ("skip_edges", C.c_int64),
     ]
 
     def as_dict(self) -> dict:

@@ -66,6 +66,8 @@ def test_info_is_consistent():
     assert 1 <= inf["mask_slices_unique"] <= inf["n_classes"] * n_slices
     assert inf["sliced_mask_bytes"] < inf["mask_table_bytes"]
     assert inf["bound_mask_layout"] == 0
+    # skip edges exist on this grammar, so the host-walk parity tests take them
+    assert inf["skip_edges"] > 0
     clf = Classifier(wl.grammar, wl.vocab)
     lib = psc.lib()
     flat, sliced = (lib.psc_device_bytes_ex(clf._h, f) for f in (psc.BIND_FLAT, psc.BIND_SLICED))
