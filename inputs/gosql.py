@@ -3,7 +3,7 @@
 Stand-in for the paper's programming-language workloads at their scale
 (Java, Go and SQL from The Stack, Sec. 4.1; their preprocessing cost,
 Tab. preprocess), whose grammars and data are not available here.  The
-grammar is written for this build and is LALR(1) as written:
+grammar is our own and is LALR(1) as written:
 
 * Go-like declarations and statements: package/import, func and method
   declarations, var/const/type declarations with struct and interface
