@@ -13,7 +13,7 @@ from typing import Callable
 
 import numpy as np
 
-from . import documents, grammars, gosql, pylike, schema, vocab
+from . import documents, grammars, gosql, pylike, pylike_core, schema, vocab
 from .grammar import GrammarTables
 from .native import HostParser
 from .seeds import rng_for
@@ -153,7 +153,7 @@ def _c4_doc(rng, wl):
 PYLIKE = _register(Workload(
     3, "pylike", B=128, steps=500, logits_dtype="bf16", logits_std=2.0,
     make_grammar=pylike.grammar, make_vocab=_c4_vocab, make_document=_c4_doc, doc_pool=2048,
-    description="Python-like CFG (88 terminals, 14 binary precedence levels, INDENT/DEDENT); "
+    description="Python-like CFG (96 terminals, 144 nonterminals, 14 binary precedence levels, INDENT/DEDENT); "
                 "a quarter of the documents nest without closing (stack depth up to ~200); "
                 "V=128,256; B=128; bf16 N(0,2)"))
 
@@ -178,17 +178,18 @@ class _DeepWorkload(Workload):
 
 
 def _c5_vocab(g):
-    return pylike.pylike_vocab(rng_for(4, salt=0x70C), 262144)
+    return pylike_core.pylike_vocab(rng_for(4, salt=0x70C), 262144)
 
 
 def _c5_doc(rng, wl):
-    return pylike.deep_program(rng, approx_chars=4500)
+    return pylike_core.deep_program(rng, approx_chars=4500)
 
 
 STRESS = _register(_DeepWorkload(
     4, "stress", B=256, steps=1000, logits_dtype="bf16", logits_std=2.0,
-    make_grammar=pylike.grammar, make_vocab=_c5_vocab, make_document=_c5_doc, doc_pool=256,
-    description="Python-like CFG, deep nesting (stack depth ~ U{1..1000}); V=262,144; B=256; bf16 N(0,2)"))
+    make_grammar=pylike_core.grammar, make_vocab=_c5_vocab, make_document=_c5_doc, doc_pool=256,
+    description="the core of the Python-like CFG (88 terminals, 80 nonterminals), deep nesting (stack depth "
+                "~ U{1..1000}); V=262,144; B=256; bf16 N(0,2)"))
 
 
 def _c6_vocab(g):
