@@ -392,7 +392,7 @@ def main():
             "bound": "hbm", "kernel": kname,
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(wl.name, kname) if fast else None,
+            "traffic": measured_traffic(wl, kname) if fast else None,
             "algorithmic_bytes_per_launch": round(bytes_fused),
             "avg_launch_us": round(lat_us, 3),
             "timing": "HIP events on the bench stream around the timed loop; one launch per step",
@@ -409,7 +409,7 @@ def main():
             "bound": "hbm", "kernel": kname,
             "achieved": round(achieved_apply, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved_apply / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(wl.name, kname) if fast else None,
+            "traffic": measured_traffic(wl, kname) if fast else None,
             "algorithmic_bytes_per_launch": round(bytes_apply_solo),
             "avg_launch_us": round(t_apply, 3),
             "timing": "HIP events around 1000 back-to-back launches of the kernel alone on the bench stream",
@@ -641,12 +641,22 @@ def device_code_hash() -> str:
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, kernel: str):
+def workload_fingerprint(wl) -> str:
+    """sha256 (first 16 hex digits) of what defines a workload's shape: its
+    grammar's sizes, the vocabulary size and the batch.  Stored counter
+    readings are for one such definition."""
+    import hashlib
+    g = wl.grammar
+    key = f"{wl.name}|{g.n_terminals}|{g.n_nonterminals}|{g.n_lr_states}|{len(g.productions)}|{wl.V}|{wl.B}"
+    return hashlib.sha256(key.encode()).hexdigest()[:16]
+
+
+def measured_traffic(wl, kernel: str):
     """HBM bytes per launch from the committed rocprofv3 --pmc summary, or
-    None when there is none for this workload or the kernel source changed
-    since the counters were taken."""
+    None when there is none for this workload, the workload's definition
+    changed, or the kernel source changed since the counters were taken."""
     tag = {"arithmetic": "arithmetic_c1", "json": "json_c2", "schema": "schema_c3", "pylike": "pylike_c4",
-           "stress": "stress_c5"}.get(workload, workload)
+           "stress": "stress_c5"}.get(wl.name, wl.name)
     path = os.path.join(ROOT, "profiles", f"mask_kernels_{tag}_pmc_traffic.md")
     if not os.path.exists(path):
         return None
@@ -656,6 +666,8 @@ def measured_traffic(workload: str, kernel: str):
             meta = json.loads(line[len("traffic_json: "):])
     h = device_code_hash()
     if not meta or meta.get("source_sha256_16") != h or kernel not in meta.get("kernels", {}):
+        return None
+    if meta.get("workload_sha256_16") != workload_fingerprint(wl):
         return None
     return meta["kernels"][kernel]["hbm_bytes"]
 
