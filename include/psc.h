@@ -183,9 +183,10 @@ psc_status psc_build(const psc_grammar *grammar, const psc_vocab *vocab, psc_han
  * terminal matching the empty string; the message names the line),
  * PSC_E_NOT_LALR1 (the message names the first conflicts: state, terminal
  * and the two actions), PSC_E_LIMIT (the terminals' NFA over 4,000,000
- * states or the lexer DFA over 1,000,000 before minimisation; groups nested
- * deeper than 500 or more than 500 repetition operators in a row are
- * PSC_E_GRAMMAR), PSC_E_OOM.
+ * states, the lexer DFA over 1,000,000 before minimisation, or its subsets
+ * holding over 200,000,000 NFA states in all; groups nested deeper than 500
+ * or more than 500 repetition operators in a row are PSC_E_GRAMMAR),
+ * PSC_E_OOM.
  */
 typedef struct psc_compiled_grammar psc_compiled_grammar;
 psc_status psc_grammar_compile(const char *text, size_t len, psc_compiled_grammar **out);

@@ -66,6 +66,7 @@ struct CompileError {
 constexpr int kMaxRegexDepth = 500;        // nested groups in one regex
 constexpr size_t kMaxNfaStates = 4000000;  // all terminals together
 constexpr size_t kMaxDfaStates = 1000000;  // before minimisation
+constexpr size_t kMaxSubsetTotal = 200000000;   // NFA states summed over the DFA's subsets
 
 // ---------------------------------------------------------------- byte sets
 
@@ -453,33 +454,43 @@ Lexer build_lexer(const std::vector<Terminal> &terms, const std::vector<Node> &n
     }
     const int n_cls = (int)reps.size();
 
+    // subset construction; the move of a subset on a byte class is the
+    // epsilon closure of its edges' targets, taken as one search over the
+    // whole target set (one visited array, told apart by a stamp), so a move
+    // costs the size of its result and not the sum of overlapping closures
     const int n_nfa = (int)nfa.eps.size();
-    std::vector<std::vector<int>> closure(n_nfa);
-    std::vector<char> have(n_nfa, 0);
-    auto closure_of = [&](int s) -> const std::vector<int> & {
-        if (!have[s]) {
-            std::vector<int> out{s};
-            std::vector<char> seen(n_nfa, 0);
-            seen[s] = 1;
-            for (size_t k = 0; k < out.size(); k++)
-                for (int v : nfa.eps[out[k]])
-                    if (!seen[v]) {
-                        seen[v] = 1;
-                        out.push_back(v);
-                    }
-            std::sort(out.begin(), out.end());
-            closure[s] = std::move(out);
-            have[s] = 1;
-        }
-        return closure[s];
+    std::vector<uint32_t> seen(n_nfa, 0);
+    uint32_t stamp = 0;
+    size_t subset_total = 0;
+    auto close = [&](std::vector<int> &set) {
+        ++stamp;
+        std::vector<int> out;
+        out.reserve(set.size());
+        for (int v : set)
+            if (seen[v] != stamp) {
+                seen[v] = stamp;
+                out.push_back(v);
+            }
+        for (size_t k = 0; k < out.size(); k++)
+            for (int w : nfa.eps[out[k]])
+                if (seen[w] != stamp) {
+                    seen[w] = stamp;
+                    out.push_back(w);
+                }
+        std::sort(out.begin(), out.end());
+        set = std::move(out);
     };
 
     std::unordered_map<std::vector<int>, int, VecHash> ids;
     std::vector<std::vector<int>> order;
     std::vector<int> trans, acc;
-    order.push_back(closure_of(master));
-    ids.emplace(order[0], 0);
-    std::vector<char> mark(n_nfa, 0);
+    {
+        std::vector<int> s0{master};
+        close(s0);
+        subset_total = s0.size();
+        ids.emplace(s0, 0);
+        order.push_back(std::move(s0));
+    }
     for (size_t i = 0; i < order.size(); i++) {
         const std::vector<int> cur = order[i];
         int best = -1;
@@ -495,26 +506,22 @@ Lexer build_lexer(const std::vector<Terminal> &terms, const std::vector<Node> &n
             const int b = reps[c];
             std::vector<int> tgt;
             for (const auto &e : edges)
-                if (e.first->has(b))
-                    for (int v : closure_of(e.second))
-                        if (!mark[v]) {
-                            mark[v] = 1;
-                            tgt.push_back(v);
-                        }
-            for (int v : tgt) mark[v] = 0;
+                if (e.first->has(b)) tgt.push_back(e.second);
             if (tgt.empty()) {
                 trans.push_back(-1);
                 continue;
             }
-            std::sort(tgt.begin(), tgt.end());
+            close(tgt);
             auto it = ids.find(tgt);
             int j;
             if (it == ids.end()) {
                 j = (int)order.size();
+                subset_total += tgt.size();
+                if (order.size() + 1 > kMaxDfaStates || subset_total > kMaxSubsetTotal)
+                    fail(PSC_E_LIMIT, "the lexer DFA exceeds " + std::to_string(kMaxDfaStates) + " states or " +
+                                          std::to_string(kMaxSubsetTotal) + " NFA states over all its subsets");
                 ids.emplace(tgt, j);
                 order.push_back(std::move(tgt));
-                if (order.size() > kMaxDfaStates)
-                    fail(PSC_E_LIMIT, "the lexer DFA exceeds " + std::to_string(kMaxDfaStates) + " states");
             } else {
                 j = it->second;
             }
@@ -523,22 +530,36 @@ Lexer build_lexer(const std::vector<Terminal> &terms, const std::vector<Node> &n
     }
     if (acc[0] >= 0) fail(PSC_E_GRAMMAR, "terminal " + terms[acc[0]].name + " matches the empty string");
 
-    // drop states from which no accepting state is reachable (q0 kept)
+    // drop states from which no accepting state is reachable (q0 kept): a
+    // search backwards from the accepting states over the reversed moves
     int n = (int)order.size();
-    std::vector<char> live(n);
-    for (int s = 0; s < n; s++) live[s] = acc[s] >= 0;
-    for (bool changed = true; changed;) {
-        changed = false;
-        for (int s = 0; s < n; s++) {
-            if (live[s]) continue;
+    std::vector<char> live(n, 0);
+    {
+        std::vector<int> rstart(n + 1, 0), redge;
+        for (size_t k = 0; k < trans.size(); k++)
+            if (trans[k] >= 0) rstart[trans[k] + 1]++;
+        for (int s = 0; s < n; s++) rstart[s + 1] += rstart[s];
+        redge.resize(rstart[n]);
+        std::vector<int> fill(rstart.begin(), rstart.end() - 1);
+        for (int s = 0; s < n; s++)
             for (int c = 0; c < n_cls; c++) {
                 const int t = trans[(size_t)s * n_cls + c];
-                if (t >= 0 && live[t]) {
-                    live[s] = 1;
-                    changed = true;
-                    break;
-                }
+                if (t >= 0) redge[fill[t]++] = s;
             }
+        std::vector<int> work;
+        for (int s = 0; s < n; s++)
+            if (acc[s] >= 0) {
+                live[s] = 1;
+                work.push_back(s);
+            }
+        while (!work.empty()) {
+            const int t = work.back();
+            work.pop_back();
+            for (int k = rstart[t]; k < rstart[t + 1]; k++)
+                if (!live[redge[k]]) {
+                    live[redge[k]] = 1;
+                    work.push_back(redge[k]);
+                }
         }
     }
     live[0] = 1;

@@ -125,6 +125,28 @@ def test_errors_are_reported(text, status, needle):
     assert e.value.status == status and needle in str(e.value), str(e.value)
 
 
+def test_bounded_repetition_compiles_in_time_and_exactly():
+    """A move of the subset construction is one closure search over all its
+    targets: /[ab]{0,2000}c/ (2,000 nested optional copies, whose closures
+    overlap) compiles in seconds, and its DFA counts the repetition exactly."""
+    import time
+    t0 = time.time()
+    c = CompiledGrammar('%start s\nA: /[ab]{0,2000}c/\ns: A\n')
+    assert time.time() - t0 < 60
+
+    def run(text):
+        q = 0
+        for ch in text.encode():
+            q = int(c.lex_next[q, ch])
+            if q < 0:
+                return None
+        return q
+
+    q = run("ab" * 1000 + "c")
+    assert q is not None and c.lex_accept[q] == 0
+    assert run("a" * 2001) is None and run("c") is not None and run("cc") is None
+
+
 def test_build_from_text_equals_build_from_tables():
     """psc_build_from_text gives the classifier psc_build gives on the
     Python front end's tables: same sizes and the same class rows for the
