@@ -58,6 +58,9 @@ def main():
                     help="PSC_OPT_SPECULATE: the fused step loads the predicted class's data during the walk")
     ap.add_argument("--no-prequeue", action="store_true",
                     help="time loops without first queueing them behind a device-side delay")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="sequences per step instead of the workload's own B (a sweep over batch sizes; the "
+                         "prefixes of sequences past B are drawn the same way; labelled in config)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
@@ -72,6 +75,12 @@ def main():
 
     dev = torch.device("cuda:0")
     wl = configs.get(args.workload)
+    if args.batch is not None:
+        import dataclasses
+        if not 1 <= args.batch <= 65535:
+            print(json.dumps({"error": "--batch must be in 1..65535"}))
+            sys.exit(2)
+        wl = dataclasses.replace(wl, B=args.batch)
     B, V = wl.B, wl.V
     W = (V + 31) // 32
     s_logit = 2 if wl.logits_dtype == "bf16" else 4
@@ -461,6 +470,7 @@ def main():
             "workload": f"{wl.name}: {wl.description}",
             "B": B, "V": V, "logits": wl.logits_dtype, "distinct_steps": n_distinct,
             "logits_pool_buffers": n_pool, "warm_cache": bool(args.warm_cache),
+            "batch_override": args.batch is not None,
         },
         "step_mode": args.mode,
         "other_mode_step_us": {("two_launch" if args.mode == "fused" else "fused"): round(t_other, 3),
