@@ -58,6 +58,9 @@ def main():
                     help="PSC_OPT_SPECULATE: the fused step loads the predicted class's data during the walk")
     ap.add_argument("--no-prequeue", action="store_true",
                     help="time loops without first queueing them behind a device-side delay")
+    ap.add_argument("--latency-probe", action="store_true",
+                    help="instead of the step: ns per dependent load (the walk's load kinds) against the table's "
+                         "size, in this workload's launch shape (libpsc_probe.so); prints one JSON line")
     ap.add_argument("--batch", type=int, default=None,
                     help="sequences per step instead of the workload's own B (a sweep over batch sizes; the "
                          "prefixes of sequences past B are drawn the same way; labelled in config)")
@@ -85,6 +88,19 @@ def main():
     W = (V + 31) // 32
     s_logit = 2 if wl.logits_dtype == "bf16" else 4
     log(f"workload {wl.name}: B={B} V={V} dtype={wl.logits_dtype}")
+
+    if args.latency_probe:
+        from paper_2608_03065_amd.probe import chase_latency
+        stream = torch.cuda.Stream(device=dev)     # default priority
+        grid = ((W + 255) // 256, B)              # the fused step's grid for bf16 logits
+        res = chase_latency(dev, stream, grid)
+        print(json.dumps({"latency_probe": res, "config": {"workload": wl.name, "grid": list(grid),
+                                                           "dependent_loads": 8, "launches": 500},
+                          "note": "per extra dependent load: (t(8) - t(0)) / 8 over back-to-back launches, each "
+                                  "starting its chains at other rows of a table of random 1 KiB rows; wave_1KiB is "
+                                  "a sparse row's or chain's load, scalar_8B a dense row's entry; with_stores adds "
+                                  "the step's 16 KiB per workgroup of nontemporal stores"}), flush=True)
+        return
 
     t0 = time.time()
     clf = Classifier(wl.grammar, wl.vocab)

@@ -1,5 +1,5 @@
 """Build libpsc.so in-tree: host construction and persistence (g++, zlib) +
-gfx950 device code (hipcc)."""
+gfx950 device code (hipcc); and libpsc_probe.so, a measurement aid."""
 from __future__ import annotations
 
 import os
@@ -9,6 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libpsc.so")
+PROBE_LIB = os.path.join(HERE, "libpsc_probe.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
@@ -42,8 +43,12 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", host_obj, store_obj, gram_obj, dev_obj, "-lz", "-o", tmp])
     os.replace(tmp, LIB)
+    # the measurement aid beside it (dependent-load latency; bench.py --latency-probe)
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-shared", os.path.join(CSRC, "psc_probe.hip"), "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, PROBE_LIB)
     return LIB
 
 

@@ -280,3 +280,22 @@ def test_host_state_errors():
     assert e.value.status == -7
     with pytest.raises(ValueError):
         clf.host_state("1+2")
+
+
+def test_probe_library_exports_and_checks_its_arguments():
+    """libpsc_probe.so (the dependent-load latency aid) exports what
+    include/psc_probe.h declares and rejects bad arguments before any launch
+    (no GPU is touched by these calls)."""
+    from paper_2608_03065_amd import probe
+    src = open(os.path.join(ROOT, "include", "psc_probe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = sorted(set(re.findall(r"\b(psc_[a-z_]+)\s*\(", src)))
+    assert names == ["psc_probe_chase"]
+    L = probe.lib()
+    tab = C.create_string_buffer(1024)
+    bad = [(2, None, tab, 1, 1, 0, 1, 1), (0, None, None, 1, 1, 0, 1, 1), (0, None, tab, 0, 1, 0, 1, 1),
+           (0, None, tab, 1, -1, 0, 1, 1), (0, None, tab, 1, 1, 0, 1, 70000), (0, None, tab, 1, 1, 1, 1, 1),
+           (1, None, tab, 1, 1, 0, 1 << 13, 1 << 12)]
+    for mode, out, t, n_rows, k, fill, gx, gy in bad:
+        assert L.psc_probe_chase(mode, out, C.cast(t, C.c_void_p) if t is not None else None, n_rows, k, fill,
+                                 gx, gy, 0, None) == 1      # hipErrorInvalidValue
