@@ -194,8 +194,12 @@ int64_t check_loaded(const psc_handle &h) {
             len = kRowHeader + 2 * (int64_t)h.n_lr;
         } else {
             if (row[4] != kSymNone || !ref_ok(row[5])) bad("sparse row default");
-            for (int32_t e = 0; e < row[1]; e++)
-                if (!ref_ok(row[kSparseHeader + kSparseEdge * e + 1])) bad("sparse row ref");
+            for (int32_t e = 0; e < row[1]; e++) {
+                const int32_t *en = row + kSparseHeader + kSparseEdge * e;
+                if (!ref_ok(en[1])) bad("sparse row ref");
+                // in range and strictly increasing: the host walk searches them by bisection
+                if (en[0] < 0 || en[0] >= h.n_lr || (e > 0 && en[0] <= en[-kSparseEdge])) bad("sparse row symbols");
+            }
             len = kSparseHeader + kSparseEdge * (int64_t)row[1];
         }
         pos += (len + 3) & ~3;

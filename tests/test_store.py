@@ -118,11 +118,24 @@ def test_crafted_tables_are_rejected(built_host, tmp_path):
         "ref into the middle of a row": lambda t: t.__setitem__(
             0, next(int(t[q]) for q in range(n_lex) if t[q] >= 0 and (t[q] & 3) == 0) + 4),
         "ref to a jump entry": lambda t: _point_at_jump(t, first_chain_ref(t)),
+        "sparse row symbols out of order": lambda t: _sparse_edges(t, n_lex, lambda e: (e[1], e[0])),
+        "sparse row symbol out of range": lambda t: _sparse_edges(
+            t, n_lex, lambda e: (info["n_lr_states"] + 5, e[1])),
     }
     for name, fn in cases.items():
         bad = tmp_path / "bad.psc"
         bad.write_bytes(_patch_table(raw, fn))
         _expect(bad, E_FORMAT)
+
+
+def _sparse_edges(t, n_lex, change):
+    """Rewrite the first two edge symbols of the first sparse row that has
+    at least two edges (every row of this table is sparse)."""
+    pos = (n_lex + 3) & ~3
+    while int(t[pos + 1]) < 2:
+        pos += (8 + 4 * int(t[pos + 1]) + 3) & ~3
+    a, b = change((int(t[pos + 8]), int(t[pos + 12])))
+    t[pos + 8], t[pos + 12] = a, b
 
 
 def _point_at_jump(t, q):
