@@ -96,9 +96,10 @@ def test_damaged_files(built_host, tmp_path):
     _expect(tmp_path / "flip.psc", E_FORMAT)
 
 
-def test_crafted_tables_are_rejected(built_host, tmp_path):
+@pytest.mark.parametrize("name", ["arithmetic", "json"])
+def test_crafted_tables_are_rejected(built_host, tmp_path, name):
     """Checksums intact, structure wrong: the validator must refuse each."""
-    wl, clf = built_host("arithmetic")
+    wl, clf = built_host(name)
     p = tmp_path / "a.psc"
     clf.save(str(p))
     raw = p.read_bytes()
@@ -122,7 +123,7 @@ def test_crafted_tables_are_rejected(built_host, tmp_path):
         "sparse row symbol out of range": lambda t: _sparse_edges(
             t, n_lex, lambda e: (info["n_lr_states"] + 5, e[1])),
     }
-    for name, fn in cases.items():
+    for case, fn in cases.items():
         bad = tmp_path / "bad.psc"
         bad.write_bytes(_patch_table(raw, fn))
         _expect(bad, E_FORMAT)
